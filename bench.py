@@ -1,0 +1,313 @@
+#!/usr/bin/env python3
+"""Benchmark of speculative-round attention on one MI355X.
+
+A step is one pass of the hot path over one synthetic batch already resident
+in HBM:
+  * verify workloads: plan -> verify partial attention -> combine;
+  * draft workloads:  the k sequential draft-step attention calls;
+  * the fp8 round:    k draft-step calls, then the verify call.
+The default workload is the variable-length paged bf16 verify batch (B=256,
+contexts log-uniform in [512, 65536], k=4, 32 query / 8 KV heads, head dim
+128, 16-token pages in shuffled physical order).
+
+Prints ONE JSON line: value = algorithmic HBM bytes per step / time per step
+(GB/s), plus verified tokens/s, the roofline of the dominant kernel (its
+average duration from HIP events recorded around each of its launches on the
+launch stream) and the CPU oracle timed on a bounded sample of the same batch.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import torch
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+from paper_2504_06419_amd import spire  # noqa: E402
+from paper_2504_06419_amd import workloads as W  # noqa: E402
+
+METRIC = "KV-attention HBM GB/s (% of peak) + verified tokens/s per round, 1 MI355X"
+HBM_PEAK_GBS = 8000.0
+DEFAULT_WORKLOAD = "verify_varlen_paged_bf16_B256"
+ELEM = {"f32": 4, "bf16": 2, "fp8": 1}
+
+
+# ---------------------------------------------------------------------------
+# algorithmic bytes: visible K+V at storage dtype + Q + fp32 output + lse +
+# lengths + page-table entries + scales
+# ---------------------------------------------------------------------------
+def verify_bytes(inp: W.VerifyInputs) -> int:
+    s = inp.spec
+    n = inp.kv_lens.tolist()
+    kv = 2 * sum(n) * s.Hkv * s.D * ELEM[s.kv_dtype]
+    q = s.B * (s.k + 1) * s.Hq * s.D * ELEM[s.q_dtype]
+    out = s.B * (s.k + 1) * s.Hq * (s.D + 1) * 4
+    meta = 4 * s.B
+    if s.page_size:
+        meta += 4 * sum((x + s.page_size - 1) // s.page_size for x in n)
+    if s.kv_dtype == "fp8":
+        meta += 8 * s.Hkv
+    return kv + q + out + meta
+
+
+def draft_step_bytes(inp: W.DraftInputs, step: int) -> int:
+    s = inp.spec
+    vis = 0
+    for L in inp.base_lens:
+        m = L + step + 1
+        vis += min(m, s.S) + max(0, min(m - s.S, s.W))
+    kv = 2 * vis * s.Hkv * s.D * ELEM[s.kv_dtype]
+    q = s.B * s.Hq * s.D * ELEM[s.q_dtype]
+    out = s.B * s.Hq * (s.D + 1) * 4
+    meta = 8 * s.B + (8 * s.Hkv if s.kv_dtype == "fp8" else 0)
+    return kv + q + out + meta
+
+
+def verify_flops(inp: W.VerifyInputs) -> int:
+    s = inp.spec
+    return 4 * (s.k + 1) * (s.Hq // s.Hkv) * s.D * s.Hkv * sum(inp.kv_lens.tolist())
+
+
+# ---------------------------------------------------------------------------
+def build_workload(name: str, dev):
+    wl = W.named_workloads()[name]
+    seed = W.MASTER_SEED + W.WORKLOAD_INDEX[name]
+    v = W.make_verify_inputs(wl["verify"], seed, device=dev, poison=None) if "verify" in wl else None
+    d = W.make_draft_inputs(wl["draft"], seed, device=dev, poison=None) if "draft" in wl else None
+    return wl, v, d
+
+
+def make_step(v, d):
+    """Return (step_fn, bytes_per_step, tokens_per_step, dominant kernel id)."""
+    calls, nbytes = [], 0
+    tokens = 0
+    dominant = None
+    if d is not None:
+        s = d.spec
+        sink = spire.kv_view(d.sink_k, d.sink_v, k_scale=d.k_scale, v_scale=d.v_scale)
+        ring = spire.kv_view(d.ring_k, d.ring_v, k_scale=d.k_scale, v_scale=d.v_scale)
+        ws = spire.workspace(spire.draft_workspace_size(s.B, s.Hq, s.Hkv, s.D))
+        out = torch.empty((s.B, s.Hq, s.D), dtype=torch.float32, device=d.q.device)
+        lse = torch.empty((s.B, s.Hq), dtype=torch.float32, device=d.q.device)
+        qs = [d.q[t].contiguous() for t in range(s.steps)]
+        lens = [d.seq_lens(t) for t in range(s.steps)]
+        for t in range(s.steps):
+            calls.append(lambda t=t: spire.draft_sparse_attn(qs[t], sink, ring, lens[t],
+                                                             d.ring_offset, s.S, s.W, d.sm_scale,
+                                                             s.Hkv, out=out, lse=lse, ws=ws))
+            nbytes += draft_step_bytes(d, t)
+        tokens = s.B * s.steps
+        dominant = "draft_partial"
+    if v is not None:
+        s = v.spec
+        kv = spire.kv_view(v.k_cache, v.v_cache, v.block_table, v.page_size, v.k_scale, v.v_scale)
+        ws = spire.workspace(spire.verify_workspace_size(s.B, s.Hq, s.Hkv, s.D, s.k))
+        out = torch.empty((s.B, s.k + 1, s.Hq, s.D), dtype=torch.float32, device=v.q.device)
+        lse = torch.empty((s.B, s.k + 1, s.Hq), dtype=torch.float32, device=v.q.device)
+        calls.append(lambda: spire.verify_attn(v.q, kv, v.kv_lens, s.Hkv, s.k, v.sm_scale, out=out,
+                                               lse=lse, ws=ws))
+        nbytes += verify_bytes(v)
+        tokens = s.B * (s.k + 1)
+        if dominant is None or verify_bytes(v) > nbytes - verify_bytes(v):
+            dominant = "verify_partial"
+
+    def step():
+        for c in calls:
+            c()
+    return step, nbytes, tokens, dominant
+
+
+def dominant_bytes(v, d, dominant):
+    if dominant == "verify_partial":
+        return verify_bytes(v)
+    return sum(draft_step_bytes(d, t) for t in range(d.spec.steps)) / d.spec.steps
+
+
+# ---------------------------------------------------------------------------
+def oracle_sample_verify(v, ids):
+    from oracle import oracle as O
+    s = v.spec
+    idx = torch.tensor(ids, dtype=torch.long, device=v.q.device)
+    lens = v.kv_lens[idx]
+    q = v.q[idx]
+    if v.page_size:
+        ps = v.page_size
+        nblk = [(int(n) + ps - 1) // ps for n in lens.tolist()]
+        rows = v.block_table[idx].long()
+        pages = torch.cat([rows[i, :nblk[i]] for i in range(len(ids))])
+        kc, vc = v.k_cache.index_select(0, pages).cpu(), v.v_cache.index_select(0, pages).cpu()
+        table = torch.full((len(ids), max(nblk)), -1, dtype=torch.int32)
+        off = 0
+        for i, nb in enumerate(nblk):
+            table[i, :nb] = torch.arange(off, off + nb, dtype=torch.int32)
+            off += nb
+    else:
+        kc, vc, table, ps = v.k_cache[idx].cpu(), v.v_cache[idx].cpu(), None, 0
+    qc, lc = q.cpu(), lens.cpu()
+    ks = None if v.k_scale is None else v.k_scale.cpu()
+    vs = None if v.v_scale is None else v.v_scale.cpu()
+    t0 = time.perf_counter()
+    O.verify(qc, kc, vc, lc, s.k, v.sm_scale, ps, table, ks, vs)
+    dt = time.perf_counter() - t0
+    n = lc.tolist()
+    nbytes = (2 * sum(n) * s.Hkv * s.D * ELEM[s.kv_dtype] + len(ids) * (s.k + 1) * s.Hq * s.D *
+              (ELEM[s.q_dtype] + 4))
+    return dt, nbytes, len(ids) * (s.k + 1)
+
+
+def oracle_sample_draft(d, ids, step):
+    from oracle import oracle as O
+    s = d.spec
+    idx = torch.tensor(ids, dtype=torch.long, device=d.q.device)
+    args = [d.q[step][idx].cpu(), d.sink_k[idx].cpu(), d.sink_v[idx].cpu(), d.ring_k[idx].cpu(),
+            d.ring_v[idx].cpu(), d.seq_lens(step)[idx].cpu(), d.ring_offset[idx].cpu()]
+    ks = None if d.k_scale is None else d.k_scale.cpu()
+    vs = None if d.v_scale is None else d.v_scale.cpu()
+    t0 = time.perf_counter()
+    O.draft(*args, s.S, s.W, d.sm_scale, ks, vs)
+    dt = time.perf_counter() - t0
+    vis = sum(min(d.base_lens[b] + step + 1, s.S) + max(0, min(d.base_lens[b] + step + 1 - s.S, s.W))
+              for b in ids)
+    nbytes = 2 * vis * s.Hkv * s.D * ELEM[s.kv_dtype] + len(ids) * s.Hq * s.D * (ELEM[s.q_dtype] + 4)
+    return dt, nbytes, len(ids)
+
+
+def run_cpu_baseline(v, d, budget_s: float):
+    from oracle import oracle as O
+    cores = O.threads()
+    g = torch.Generator().manual_seed(0)
+    total_t, total_b, total_tok, used = 0.0, 0, 0, []
+    if v is not None:
+        order = torch.randperm(v.spec.B, generator=g).tolist()
+        chunk = max(1, cores // max(1, v.spec.Hkv) + 1)
+        pos = 0
+        while total_t < budget_s and pos < len(order):
+            ids = order[pos:pos + chunk]
+            pos += chunk
+            dt, nb, tok = oracle_sample_verify(v, ids)
+            total_t += dt; total_b += nb; total_tok += tok; used += ids
+        kind = f"verify rows of {len(used)} of {v.spec.B} sequences (seeded choice)"
+        unit_tokens = "verified tokens/s"
+    else:
+        order = torch.randperm(d.spec.B, generator=g).tolist()
+        chunk = max(1, cores // max(1, d.spec.Hkv) + 1)
+        pos = 0
+        while total_t < budget_s and pos < len(order):
+            ids = order[pos:pos + chunk]
+            pos += chunk
+            dt, nb, tok = oracle_sample_draft(d, ids, 0)
+            total_t += dt; total_b += nb; total_tok += tok; used += ids
+        kind = f"draft step 0 of {len(used)} of {d.spec.B} sequences (seeded choice)"
+        unit_tokens = "drafted tokens/s"
+    return {"value": total_b / total_t / 1e9, "unit": "GB/s", "cores": cores, "kind": "oracle",
+            "sample": kind, "seconds": round(total_t, 3),
+            "tokens_per_s": total_tok / total_t, "tokens_unit": unit_tokens}
+
+
+# ---------------------------------------------------------------------------
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD, choices=list(W.named_workloads()))
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--traffic-json", default=os.path.join(ROOT, "profiles", "traffic.json"))
+    a = ap.parse_args()
+    if a.gpus != 1:
+        print(f"bench.py measures one GPU only (asked for --gpus {a.gpus}); the multi-GPU sharding "
+              "of this path is described in DESIGN.md and is not run.", file=sys.stderr)
+        sys.exit(2)
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    spire.load()
+    print(f"[bench] building workload {a.workload}", file=sys.stderr, flush=True)
+    wl, v, d = build_workload(a.workload, dev)
+    step, nbytes, tokens, dominant = make_step(v, d)
+    torch.cuda.synchronize()
+
+    print(f"[bench] warmup {a.warmup}", file=sys.stderr, flush=True)
+    for _ in range(a.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    # timed region: exactly K steps between two events on the launch stream
+    print(f"[bench] timing {a.steps} steps", file=sys.stderr, flush=True)
+    st = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(st)
+    for _ in range(a.steps):
+        step()
+    e1.record(st)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / a.steps
+
+    # per-kernel durations (HIP events around each launch, same stream), separate pass
+    spire.timing_enable(True)
+    spire.timing_collect()
+    for _ in range(a.steps):
+        step()
+    torch.cuda.synchronize()
+    recs = spire.timing_collect()
+    spire.timing_enable(False)
+    per_kernel = {}
+    for name, t in recs:
+        per_kernel.setdefault(name, []).append(t)
+    kavg = {k: sum(x) / len(x) for k, x in per_kernel.items()}
+    dom_ms = kavg.get(dominant, float("nan"))
+    dom_bytes = dominant_bytes(v, d, dominant)
+    achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
+
+    traffic = None
+    if os.path.exists(a.traffic_json):
+        try:
+            tj = json.load(open(a.traffic_json))
+            ent = tj.get(a.workload, {})
+            if ent.get("kernel") == dominant and ent.get("bytes_per_launch"):
+                traffic = ent["bytes_per_launch"]
+        except Exception:
+            traffic = None
+
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    spec = (v or d).spec
+    cfg = {"workload": a.workload, "B": spec.B, "Hq": spec.Hq, "Hkv": spec.Hkv, "D": spec.D,
+           "kv_dtype": spec.kv_dtype}
+    if v is not None:
+        cfg.update({"k": v.spec.k, "ctx": [v.spec.ctx_lo, v.spec.ctx_hi],
+                    "page_size": v.spec.page_size, "sum_kv_len": int(sum(v.kv_lens.tolist()))})
+    if d is not None:
+        cfg.update({"S": d.spec.S, "W": d.spec.W, "draft_steps": d.spec.steps})
+    res = {
+        "metric": METRIC, "value": round(gbs, 2), "unit": "GB/s", "n_gpus": 1, "steps": a.steps,
+        "warmup": a.warmup, "ms_per_step": round(ms, 5), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": spec.kv_dtype, "data": "synthetic",
+        "config": cfg,
+        "frac_of_hbm_peak": round(gbs / HBM_PEAK_GBS, 4),
+        "tokens_per_s": round(tokens / (ms * 1e-3), 1),
+        "tokens_unit": "verified tokens/s" if v is not None else "drafted tokens/s",
+        "bytes_per_step": nbytes,
+        "kernel_ms": {k: round(x, 5) for k, x in kavg.items()},
+        "roofline": {"bound": "hbm", "kernel": dominant, "achieved": round(achieved, 2),
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "traffic": traffic, "bytes_per_launch": dom_bytes,
+                     "avg_launch_ms": round(dom_ms, 5)},
+    }
+    if not a.no_cpu_baseline:
+        print(f"[bench] cpu baseline (~{a.cpu_seconds}s)", file=sys.stderr, flush=True)
+        res["cpu_baseline"] = run_cpu_baseline(v, d, a.cpu_seconds)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,194 @@
+/*
+ * spire.h -- C ABI of the speculative-round attention library for MI355X (gfx950).
+ *
+ * A speculation round (paper Sec. 2) runs the draft model k times on one token
+ * and then the target model once on k+1 tokens in parallel; in the
+ * large-batch, long-context regime the paper targets (Sec. 1, Sec. 3.1) the
+ * cost of each of those forward passes is dominated by reading the KV cache
+ * inside attention.  This library computes exactly that attention:
+ *
+ *   spire_verify_attn        -- target verification (Sec. 2, t_verify): k+1
+ *                               queries per sequence, causal among themselves,
+ *                               over the sequence's whole variable-length,
+ *                               grouped-query KV cache (contiguous or paged).
+ *   spire_draft_sparse_attn  -- one draft step (Sec. 3.1, Sec. 4): one query per
+ *                               sequence over S attention-sink tokens plus a
+ *                               sliding window of the W most recent positions
+ *                               kept in a ring buffer (StreamingLLM mask).
+ *
+ * Attention definition used by both (the paper does not spell it out): for each
+ * visible key j, s_j = sm_scale * <q, K_j>; out = sum_j softmax(s)_j V_j and
+ * lse = ln sum_j exp(s_j).  Query head h reads KV head h / (Hq / Hkv).  A row
+ * with no visible key returns zeros and lse = -inf.
+ *
+ * Conventions for every entry point
+ *  - All data pointers are DEVICE pointers (memory of the current HIP device);
+ *    the spire_kv descriptor itself is a HOST struct read during the call.
+ *  - Every buffer is borrowed: the library never allocates device memory,
+ *    never frees, and keeps no pointer after the call returns.  Scratch memory
+ *    comes from the caller's `workspace` (sized by *_workspace_size).
+ *  - Work is enqueued on `stream` and the call returns without synchronising;
+ *    the caller keeps every buffer alive until the stream has passed it.
+ *  - Calls that share one workspace must be ordered on one stream.
+ *  - Arguments are validated on the host before anything is enqueued; invalid
+ *    input returns a status and enqueues nothing.  Device-resident values
+ *    (lengths, block tables, ring offsets) are clamped on the device to what
+ *    the descriptors allow, so no value of them can make a kernel read outside
+ *    the described storage.
+ *  - Results are deterministic: the same inputs give bitwise identical output
+ *    (fixed work partition, no floating-point atomics).
+ *  - On a non-OK status spire_last_error() returns a message for the calling
+ *    thread.
+ */
+#ifndef SPIRE_H
+#define SPIRE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SPIRE_VERSION 1
+
+typedef enum spire_dtype {
+    SPIRE_F32 = 0,        /* IEEE binary32 */
+    SPIRE_BF16 = 1,       /* bfloat16 (upper half of binary32) */
+    SPIRE_FP8_E4M3FN = 2  /* OCP 8-bit e4m3fn (bias 7, no inf, max 448), KV only */
+} spire_dtype;
+
+typedef enum spire_status {
+    SPIRE_OK = 0,
+    SPIRE_ERR_INVALID_ARG = 1,  /* null pointer, negative size, bad stride, ... */
+    SPIRE_ERR_UNSUPPORTED = 2,  /* valid request outside what the kernels implement */
+    SPIRE_ERR_WORKSPACE = 3,    /* workspace missing or smaller than *_workspace_size */
+    SPIRE_ERR_HIP = 4           /* a HIP runtime call or kernel launch failed */
+} spire_status;
+
+/*
+ * A K/V cache view.  Element (blk, h, t, d) of K lives at
+ *   k + (blk * s_blk + h * s_head + t * s_tok + d) * sizeof(dtype)
+ * and likewise for V (same strides).  d is contiguous and each row of D
+ * elements must start 16-byte aligned (strides multiples of 16 bytes).
+ *   contiguous (page_size == 0): blk = sequence index b, t = key index j,
+ *     j < capacity; `capacity` is the number of token rows per sequence.
+ *   paged (page_size > 0): blk = block_table[b * max_blocks + j / page_size],
+ *     t = j % page_size; page ids are clamped to [0, num_blocks).
+ * fp8 storage needs per-KV-head dequantisation scales: the value of a stored
+ * byte is decode(byte) * k_scale[h] (keys) or * v_scale[h] (values).
+ */
+typedef struct spire_kv {
+    const void *k;               /* device */
+    const void *v;               /* device */
+    const int32_t *block_table;  /* device [B, max_blocks] int32, paged only (else NULL) */
+    const float *k_scale;        /* device [Hkv] fp32, fp8 only (else NULL) */
+    const float *v_scale;        /* device [Hkv] fp32, fp8 only (else NULL) */
+    int64_t s_blk;               /* element strides (not bytes) */
+    int64_t s_head;
+    int64_t s_tok;
+    int32_t dtype;               /* spire_dtype */
+    int32_t page_size;           /* 0 = contiguous; paged: tokens per page */
+    int32_t max_blocks;          /* paged: columns of block_table */
+    int32_t num_blocks;          /* paged: physical pages addressable in k / v */
+    int32_t capacity;            /* contiguous: token rows per sequence */
+    int32_t reserved;            /* must be 0 */
+} spire_kv;
+
+/* Bytes of workspace spire_verify_attn needs for these sizes on the current
+ * device (0 on invalid sizes). */
+size_t spire_verify_workspace_size(int32_t B, int32_t Hq, int32_t Hkv, int32_t D, int32_t k);
+
+/*
+ * Target verification attention (paper Sec. 2: the target forward pass on the
+ * k+1 tokens of a round in parallel).
+ *   q        [B, k+1, Hq, D] contiguous, q_dtype SPIRE_F32 or SPIRE_BF16;
+ *            row i of sequence b is the last accepted token (i = 0) or draft
+ *            token i.
+ *   kv       cache of every sequence; the k+1 tokens being verified have been
+ *            appended already, so sequence b holds n_b = kv_lens[b] keys.
+ *   kv_lens  [B] int32: n_b; query i sees keys [0, n_b - k + i) (bottom-right
+ *            causal mask).  n_b >= k+1 for a full result; smaller values are
+ *            legal (rows with no visible key return zeros, lse = -inf); values
+ *            above the cache capacity are clamped to it.
+ *   sizes    B >= 0, Hkv >= 1, Hq % Hkv == 0, D in {64, 128}, 0 <= k <= 15,
+ *            (k+1) * Hq / Hkv <= 128.
+ *   sm_scale softmax scale (usually 1/sqrt(D)).
+ *   out      [B, k+1, Hq, D] contiguous, out_dtype SPIRE_F32 or SPIRE_BF16.
+ *   lse      [B, k+1, Hq] fp32 natural-log sum-exp, or NULL.
+ *   workspace >= spire_verify_workspace_size(B, Hq, Hkv, D, k) bytes of device
+ *            memory, 256-byte aligned; its contents need no initialisation.
+ * Supported storage: KV f32, bf16 or fp8 (fp8 needs k_scale and v_scale).
+ */
+spire_status spire_verify_attn(const void *q, int32_t q_dtype, const spire_kv *kv,
+                               const int32_t *kv_lens, int32_t B, int32_t Hq, int32_t Hkv,
+                               int32_t D, int32_t k, float sm_scale, void *out,
+                               int32_t out_dtype, float *lse, void *workspace,
+                               size_t workspace_bytes, hipStream_t stream);
+
+/* Bytes of workspace spire_draft_sparse_attn needs (0 on invalid sizes). */
+size_t spire_draft_workspace_size(int32_t B, int32_t Hq, int32_t Hkv, int32_t D);
+
+/*
+ * One draft step of static sparse attention (paper Sec. 3.1 and Sec. 4: a
+ * StreamingLLM mask of S sink tokens plus a window of W positions keeps the
+ * draft KV cache at constant size).
+ *   q        [B, Hq, D] contiguous: one query per sequence (f32 or bf16).
+ *   sink     contiguous view (page_size 0, capacity >= S): row p < S holds
+ *            logical position p.
+ *   ring     contiguous view (page_size 0, capacity >= W) of W slots: logical
+ *            position p >= S lives in slot (ring_offset[b] + p - S) mod W.
+ *            sink and ring have the same dtype (fp8: each view's own scales).
+ *   seq_lens [B] int32: m_b, the number of logical positions including the
+ *            query's own token (the caller has written it to the cache).
+ *            Visible positions: [0, min(S, m_b)) U [max(S, m_b - W), m_b),
+ *            each counted once.  m_b <= 0 gives zeros and lse = -inf.
+ *   ring_offset [B] int32, reduced modulo W on the device.
+ *   sizes    S >= 0, W >= 0, S + W >= 1, other sizes as for verify with k = 0.
+ *   out      [B, Hq, D]; lse [B, Hq] or NULL; workspace as for verify.
+ */
+spire_status spire_draft_sparse_attn(const void *q, int32_t q_dtype, const spire_kv *sink,
+                                     const spire_kv *ring, const int32_t *seq_lens,
+                                     const int32_t *ring_offset, int32_t B, int32_t Hq,
+                                     int32_t Hkv, int32_t D, int32_t S, int32_t W, float sm_scale,
+                                     void *out, int32_t out_dtype, float *lse, void *workspace,
+                                     size_t workspace_bytes, hipStream_t stream);
+
+/* Human-readable name of a status code (static string, never NULL). */
+const char *spire_status_string(spire_status status);
+
+/* Detail message of the last non-OK status returned on the calling thread
+ * (thread-local static storage, "" if none). */
+const char *spire_last_error(void);
+
+/* SPIRE_VERSION of the built library. */
+int32_t spire_version(void);
+
+/*
+ * Kernel selection, process-wide: 0 = automatic (matrix-core kernels where the
+ * dtype and shape allow, the generic vector kernel otherwise), 1 = always the
+ * generic vector kernel.  Returns SPIRE_ERR_INVALID_ARG for other values.
+ */
+spire_status spire_set_kernel_variant(int32_t variant);
+
+/*
+ * Per-kernel timing for measurement.  spire_timing_enable(1) creates HIP
+ * events (this allocates; call it outside timed regions) and from then on
+ * every entry point records an event pair around each kernel it launches, on
+ * the caller's stream.  spire_timing_collect waits for the recorded events,
+ * writes up to `max` (kernel id, milliseconds) pairs in launch order and
+ * returns how many it wrote, then forgets them.  Kernel ids: 0 plan,
+ * 1 verify partial attention, 2 draft partial attention, 3 combine.  At most
+ * 4096 launches are kept between collects (older ones are dropped).
+ * spire_timing_enable(0) releases the events.  Not thread-safe.
+ */
+spire_status spire_timing_enable(int32_t on);
+int32_t spire_timing_collect(int32_t *kernel_ids, float *ms, int32_t max);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SPIRE_H */

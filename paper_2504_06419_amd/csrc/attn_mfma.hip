@@ -1,0 +1,461 @@
+// attn_mfma.hip -- split-KV partial attention on CDNA4 matrix cores (gfx950).
+//
+// One wave is one worker of the stream-K partition (spire_internal.h).  For a
+// segment (sequence b, KV head h) it packs all R = (k+1) * g query rows that
+// read this KV head -- the k+1 verify tokens (paper Sec. 2) times the g query
+// heads of the group -- into 16-row blocks, so that every K/V tile is fetched
+// from HBM once and feeds all of them.  Per 32-key tile:
+//
+//   S^T (keys x rows)  = K Q^T      v_mfma_f32_16x16x32_bf16, A = K, B = Q^T
+//   online softmax in base 2 on S^T (row max across the 4 lane groups)
+//   O^T (dims x rows) += V^T P^T    v_mfma_f32_16x16x32_bf16, A = V^T, B = P^T
+//
+// Register layouts (lane l, n16 = l & 15, j = l >> 4):
+//   * MFMA A/B operands: lane l holds row/column n16 and the 8 consecutive
+//     reduction indices 8j..8j+7; C: lane l holds rows 4j..4j+3, column n16.
+//   * S^T row m of key group mb is key 16mb + 4(m&3) + (m>>2), so the C output
+//     of lane l is keys 16mb + 4i + j (i = 0..3) for row 16nb + n16.
+//   * The PV reduction index 8j+t is key 4t + j: exactly the S^T values lane l
+//     already holds (t < 4 from mb = 0, t >= 4 from mb = 1), so P never
+//     leaves its lane, and each V load instruction (t fixed) covers 4 whole,
+//     consecutive 256-byte key rows.
+//   * PV row m of dim block mb' is head dim 8m + mb', so lane l loads the 16
+//     contiguous bytes d = 8 n16 .. 8 n16 + 7 of each of its keys, transposes
+//     8 keys x 8 dims in registers (byte permutes), and ends up owning the 32
+//     contiguous output dims 32j .. 32j + 31 of its row.
+//   * K: lane l loads 64 contiguous bytes per key group row (16 B per call).
+// fp8 (OCP e4m3fn) K/V are converted to bf16 in registers (exact); the
+// per-head K scale is folded into the softmax scale, the V scale into the
+// final normalisation.  Three tiles are kept in registers (two in flight).
+#include "spire_internal.h"
+
+namespace spire {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((__vector_size__(16)));
+typedef __bf16 bf16x2 __attribute__((__vector_size__(4)));
+
+enum { MODE_CONTIG = 0, MODE_PAGED = 1, MODE_DRAFT = 2 };
+
+__device__ __forceinline__ f32x4 mfma_bf16(u32x4 a, u32x4 b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
+                                                   __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+}
+
+// two OCP e4m3fn bytes (selected half of `x`) -> two bf16 (exact, scale 1)
+template <bool HI>
+__device__ __forceinline__ uint32_t fp8x2_to_bf16x2(uint32_t x) {
+    return __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(x, 1.0f, HI));
+}
+__device__ __forceinline__ u32x4 fp8x8_to_bf16x8(uint32_t a, uint32_t b) {
+    u32x4 r;
+    r.x = fp8x2_to_bf16x2<false>(a);
+    r.y = fp8x2_to_bf16x2<true>(a);
+    r.z = fp8x2_to_bf16x2<false>(b);
+    r.w = fp8x2_to_bf16x2<true>(b);
+    return r;
+}
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+    bf16x2 v = {(__bf16)lo, (__bf16)hi};
+    return __builtin_bit_cast(uint32_t, v);
+}
+
+template <bool FP8> struct TileRegs;
+template <> struct TileRegs<false> { u32x4 k[2][4]; u32x4 v[8]; };  // bf16
+template <> struct TileRegs<true> { u32x4 k[2][2]; u32x2 v[8]; };   // fp8
+
+// Per-segment addressing state (uniform values except the per-lane offsets).
+struct SegAddr {
+    const uint8_t *kseq, *vseq;      // contiguous: (b, h) base; paged: h offset applied
+    const uint8_t *ksink, *vsink;    // draft sinks (b, h) base
+    const int32_t *table;            // paged: block table row of b
+    int64_t blk_bytes;               // paged: bytes per page (s_blk * elem)
+    int64_t tok_bytes, sink_tok_bytes;
+    int32_t n;                       // keys of the segment
+    int32_t cap16;                   // contiguous: last 16-aligned group start
+    int32_t ps, num_blocks;
+    int32_t ns, rs, W;               // draft: sinks, first ring slot, window
+};
+
+// base pointer of the 16-key group starting at key `key0` (uniform)
+template <int MODE>
+__device__ __forceinline__ int64_t group_row_offset(const SegAddr &a, int key0) {
+    if (MODE == MODE_CONTIG) {
+        const int row = key0 < a.cap16 ? key0 : a.cap16;
+        return (int64_t)row * a.tok_bytes;
+    } else {
+        const int kk = key0 < a.n ? key0 : a.n - 1;
+        int page = a.table[kk / a.ps];
+        page = page < 0 ? 0 : (page >= a.num_blocks ? a.num_blocks - 1 : page);
+        const int row = (key0 < a.n ? key0 : kk) % a.ps & ~15;
+        return (int64_t)page * a.blk_bytes + (int64_t)row * a.tok_bytes;
+    }
+}
+
+// draft: storage row of key j (per lane)
+__device__ __forceinline__ void draft_rows(const SegAddr &a, int j, const uint8_t *&kp,
+                                           const uint8_t *&vp) {
+    if (j < a.ns) {
+        kp = a.ksink + (int64_t)j * a.sink_tok_bytes;
+        vp = a.vsink + (int64_t)j * a.sink_tok_bytes;
+    } else if (a.W > 0) {
+        int s = a.rs + (j - a.ns);
+        while (s >= a.W) s -= a.W;
+        kp = a.kseq + (int64_t)s * a.tok_bytes;
+        vp = a.vseq + (int64_t)s * a.tok_bytes;
+    } else {
+        kp = a.ksink + (int64_t)(a.ns - 1) * a.sink_tok_bytes;
+        vp = a.vsink + (int64_t)(a.ns - 1) * a.sink_tok_bytes;
+    }
+}
+
+template <bool FP8, int MODE>
+__device__ __forceinline__ void load_tile(TileRegs<FP8> &T, const SegAddr &a, int tile, int lane) {
+    const int n16 = lane & 15, j = lane >> 4;
+    const int rho = 4 * (n16 & 3) + (n16 >> 2);
+    const int key0 = tile * kMfmaTile;
+    if (MODE == MODE_DRAFT) {
+#pragma unroll
+        for (int mb = 0; mb < 2; ++mb) {
+            const uint8_t *kp, *vp;
+            draft_rows(a, key0 + 16 * mb + rho, kp, vp);
+            if (FP8) {
+#pragma unroll
+                for (int u = 0; u < 2; ++u)
+                    T.k[mb][u] = *reinterpret_cast<const u32x4 *>(kp + 64 * u + 16 * j);
+            } else {
+#pragma unroll
+                for (int c = 0; c < 4; ++c)
+                    T.k[mb][c] = *reinterpret_cast<const u32x4 *>(kp + 64 * c + 16 * j);
+            }
+        }
+#pragma unroll
+        for (int t = 0; t < 8; ++t) {
+            const uint8_t *kp, *vp;
+            draft_rows(a, key0 + 4 * t + j, kp, vp);
+            if (FP8)
+                *reinterpret_cast<u32x2 *>(&T.v[t]) = *reinterpret_cast<const u32x2 *>(vp + 8 * n16);
+            else
+                *reinterpret_cast<u32x4 *>(&T.v[t]) = *reinterpret_cast<const u32x4 *>(vp + 16 * n16);
+        }
+    } else {
+        const int64_t g0 = group_row_offset<MODE>(a, key0);
+        const int64_t g1 = group_row_offset<MODE>(a, key0 + 16);
+        const int64_t koff = (int64_t)rho * a.tok_bytes + 16 * j;
+#pragma unroll
+        for (int mb = 0; mb < 2; ++mb) {
+            const uint8_t *kp = a.kseq + (mb ? g1 : g0) + koff;
+            if (FP8) {
+#pragma unroll
+                for (int u = 0; u < 2; ++u) T.k[mb][u] = *reinterpret_cast<const u32x4 *>(kp + 64 * u);
+            } else {
+#pragma unroll
+                for (int c = 0; c < 4; ++c) T.k[mb][c] = *reinterpret_cast<const u32x4 *>(kp + 64 * c);
+            }
+        }
+        const int64_t voff = (int64_t)j * a.tok_bytes + (FP8 ? 8 : 16) * n16;
+#pragma unroll
+        for (int t = 0; t < 8; ++t) {
+            const uint8_t *vp = a.vseq + (t < 4 ? g0 : g1) + (int64_t)(4 * (t & 3)) * a.tok_bytes + voff;
+            if (FP8)
+                *reinterpret_cast<u32x2 *>(&T.v[t]) = *reinterpret_cast<const u32x2 *>(vp);
+            else
+                *reinterpret_cast<u32x4 *>(&T.v[t]) = *reinterpret_cast<const u32x4 *>(vp);
+        }
+    }
+}
+
+template <int NB> struct SoftmaxState {
+    f32x4 acc[8][NB];
+    float m[NB];
+    float l[NB];
+    int lim[NB];
+};
+
+template <bool FP8, int NB>
+__device__ __forceinline__ void compute_tile(TileRegs<FP8> &T, const u32x4 (&qf)[NB][4],
+                                             SoftmaxState<NB> &st, int tile, int n, int full_lim,
+                                             float sc, int lane) {
+    const int j = lane >> 4;
+    const int key0 = tile * kMfmaTile;
+
+    // ---- S^T = K Q^T -------------------------------------------------------
+    f32x4 s[2][NB];
+#pragma unroll
+    for (int mb = 0; mb < 2; ++mb) {
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) s[mb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            u32x4 kf;
+            if (FP8) {
+                const u32x4 raw = T.k[mb][c >> 1];
+                kf = (c & 1) ? fp8x8_to_bf16x8(raw.z, raw.w) : fp8x8_to_bf16x8(raw.x, raw.y);
+            } else {
+                kf = T.k[mb][c];
+            }
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb) s[mb][nb] = mfma_bf16(kf, qf[nb][c], s[mb][nb]);
+        }
+    }
+
+    // ---- mask, online softmax (base 2) ---------------------------------------
+    const bool need_mask = key0 + kMfmaTile > full_lim;
+    u32x4 pb[NB];
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+        float x[2][4];
+        float mx = -INFINITY;
+#pragma unroll
+        for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                float v = s[mb][nb][i] * sc;
+                if (need_mask && key0 + 16 * mb + 4 * i + j >= st.lim[nb]) v = -INFINITY;
+                x[mb][i] = v;
+                mx = fmaxf(mx, v);
+            }
+        mx = fmaxf(mx, __shfl_xor(mx, 16));
+        mx = fmaxf(mx, __shfl_xor(mx, 32));
+        const float mnew = fmaxf(st.m[nb], mx);
+        const float msub = mnew == -INFINITY ? 0.f : mnew;
+        const float alpha = exp2f(st.m[nb] - msub);  // m = -inf -> 0
+        st.m[nb] = mnew;
+        float psum = 0.f;
+#pragma unroll
+        for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                x[mb][i] = exp2f(x[mb][i] - msub);
+                psum += x[mb][i];
+            }
+        st.l[nb] = st.l[nb] * alpha + psum;
+#pragma unroll
+        for (int mb = 0; mb < 8; ++mb) st.acc[mb][nb] *= alpha;
+        pb[nb].x = pack_bf16x2(x[0][0], x[0][1]);
+        pb[nb].y = pack_bf16x2(x[0][2], x[0][3]);
+        pb[nb].z = pack_bf16x2(x[1][0], x[1][1]);
+        pb[nb].w = pack_bf16x2(x[1][2], x[1][3]);
+    }
+
+    // ---- V: keys beyond the segment end are zeroed (storage there may be anything)
+    u32x4 vb[8];
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+        if (FP8) {
+            const u32x2 raw = *reinterpret_cast<const u32x2 *>(&T.v[t]);
+            vb[t] = fp8x8_to_bf16x8(raw.x, raw.y);
+        } else {
+            vb[t] = *reinterpret_cast<const u32x4 *>(&T.v[t]);
+        }
+        if (key0 + kMfmaTile > n && key0 + 4 * t + j >= n) vb[t] = u32x4{0u, 0u, 0u, 0u};
+    }
+
+    // ---- O^T += V^T P^T -------------------------------------------------------
+#pragma unroll
+    for (int mb = 0; mb < 8; ++mb) {
+        const int w = mb >> 1;
+        u32x4 a;
+        if (mb & 1) {
+            a.x = (vb[0][w] >> 16) | (vb[1][w] & 0xffff0000u);
+            a.y = (vb[2][w] >> 16) | (vb[3][w] & 0xffff0000u);
+            a.z = (vb[4][w] >> 16) | (vb[5][w] & 0xffff0000u);
+            a.w = (vb[6][w] >> 16) | (vb[7][w] & 0xffff0000u);
+        } else {
+            a.x = (vb[0][w] & 0xffffu) | (vb[1][w] << 16);
+            a.y = (vb[2][w] & 0xffffu) | (vb[3][w] << 16);
+            a.z = (vb[4][w] & 0xffffu) | (vb[5][w] << 16);
+            a.w = (vb[6][w] & 0xffffu) | (vb[7][w] << 16);
+        }
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) st.acc[mb][nb] = mfma_bf16(a, pb[nb], st.acc[mb][nb]);
+    }
+}
+
+template <bool FP8, int NB, int MODE>
+__global__ __launch_bounds__(256, 1) void mfma_partial_kernel(Problem p, Plan pl) {
+    const int lane = threadIdx.x & 63;
+    const int n16 = lane & 15, j = lane >> 4;
+    const int wid = __builtin_amdgcn_readfirstlane(blockIdx.x * kMfmaWavesPerWG + (threadIdx.x >> 6));
+    if (wid >= pl.workers) return;
+    const int64_t T = (int64_t)pl.prefix[p.B] * pl.units;
+    int64_t pos = worker_begin(wid, T, pl.workers);
+    const int64_t end = worker_begin(wid + 1, T, pl.workers);
+    if (pos >= end) return;
+    int seg = pl.wstart[2 * wid];
+    int tile = pl.wstart[2 * wid + 1];
+    const int64_t begin = pos;
+
+    while (pos < end) {
+        const int b = seg / pl.units;
+        const int h = seg - b * pl.units;
+        const int tiles_b = pl.prefix[b + 1] - pl.prefix[b];
+        const int64_t left = end - pos;
+        const int t1 = left < (int64_t)(tiles_b - tile) ? tile + (int)left : tiles_b;
+        const int n = pl.nkeys[b];
+
+        // ---- segment addressing ------------------------------------------------
+        SegAddr a;
+        a.n = n;
+        a.tok_bytes = p.kv.s_tok * p.kv.elem;
+        if (MODE == MODE_PAGED) {
+            a.kseq = p.kv.k + (int64_t)h * p.kv.s_head * p.kv.elem;
+            a.vseq = p.kv.v + (int64_t)h * p.kv.s_head * p.kv.elem;
+            a.table = p.kv.block_table + (int64_t)b * p.kv.max_blocks;
+            a.blk_bytes = p.kv.s_blk * p.kv.elem;
+            a.ps = p.kv.page_size;
+            a.num_blocks = p.kv.num_blocks;
+        } else {
+            const int64_t off = ((int64_t)b * p.kv.s_blk + (int64_t)h * p.kv.s_head) * p.kv.elem;
+            a.kseq = p.kv.k + off;
+            a.vseq = p.kv.v + off;
+            a.cap16 = p.kv.capacity - 16;
+        }
+        if (MODE == MODE_DRAFT) {
+            const int64_t soff = ((int64_t)b * p.sink.s_blk + (int64_t)h * p.sink.s_head) * p.sink.elem;
+            a.ksink = p.sink.k + soff;
+            a.vsink = p.sink.v + soff;
+            a.sink_tok_bytes = p.sink.s_tok * p.sink.elem;
+            const int m = p.lens[b] < 0 ? 0 : p.lens[b];
+            a.ns = m < p.S ? m : p.S;
+            a.W = p.W;
+            int first = m - p.S - p.W;  // first valid logical ring index
+            first = first < 0 ? 0 : first;
+            int o = 0;
+            if (p.W > 0) {
+                o = p.ring_offset[b] % p.W;
+                if (o < 0) o += p.W;
+                o = (n - a.ns == p.W) ? 0 : (o + first % p.W) % p.W;  // full ring: physical order
+            }
+            a.rs = o;
+        }
+
+        // ---- queries: rows 16nb + n16, packed as MFMA B operands ---------------
+        u32x4 qf[NB][4];
+        SoftmaxState<NB> st;
+        const int full_lim = p.draft ? n : n - p.k;
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) {
+            const int r = 16 * nb + n16;
+            st.m[nb] = -INFINITY;
+            st.l[nb] = 0.f;
+            st.lim[nb] = r < p.R ? visible_limit(p, n, r) : n;
+#pragma unroll
+            for (int mb = 0; mb < 8; ++mb) st.acc[mb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                const int d0 = FP8 ? 64 * (c >> 1) + 16 * j + 8 * (c & 1) : 32 * c + 8 * j;
+                if (r < p.R)
+                    qf[nb][c] = *reinterpret_cast<const u32x4 *>(p.q + (row_offset(p, b, h, r) + d0) * 2);
+                else
+                    qf[nb][c] = u32x4{0u, 0u, 0u, 0u};
+            }
+        }
+        float sc = p.sm_scale_log2;
+        if (FP8) sc *= p.kv.k_scale[h];
+
+        // ---- tiles [tile, t1): three register buffers, two tiles in flight ----
+        if (n > 0) {
+            TileRegs<FP8> A, Bt, C;
+            const int last = t1 - 1;
+            load_tile<FP8, MODE>(A, a, tile, lane);
+            load_tile<FP8, MODE>(Bt, a, tile + 1 < last ? tile + 1 : last, lane);
+            int tt = tile;
+            while (true) {
+                load_tile<FP8, MODE>(C, a, tt + 2 < last ? tt + 2 : last, lane);
+                compute_tile<FP8, NB>(A, qf, st, tt, n, full_lim, sc, lane);
+                if (++tt > last) break;
+                load_tile<FP8, MODE>(A, a, tt + 2 < last ? tt + 2 : last, lane);
+                compute_tile<FP8, NB>(Bt, qf, st, tt, n, full_lim, sc, lane);
+                if (++tt > last) break;
+                load_tile<FP8, MODE>(Bt, a, tt + 2 < last ? tt + 2 : last, lane);
+                compute_tile<FP8, NB>(C, qf, st, tt, n, full_lim, sc, lane);
+                if (++tt > last) break;
+            }
+        }
+
+        // ---- finalize: reduce the row sums over the 4 lane groups --------------
+        const bool whole = (tile == 0 && t1 == tiles_b);
+        const int64_t slot = 2 * (int64_t)wid + (pos == begin ? 0 : 1);
+        const float vs = FP8 ? p.kv.v_scale[h] : 1.f;
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) {
+            float l = st.l[nb];
+            l += __shfl_xor(l, 16);
+            l += __shfl_xor(l, 32);
+            const int r = 16 * nb + n16;
+            if (r >= p.R) continue;
+            const float inv = l > 0.f ? vs / l : 0.f;
+            const float lse2 = l > 0.f ? st.m[nb] + log2f(l) : -INFINITY;
+            if (whole) {
+                const int64_t off = row_offset(p, b, h, r) + 32 * j;
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    if (p.out_dtype == SPIRE_BF16) {
+                        u32x4 o;
+                        o.x = pack_bf16x2(st.acc[0][nb][i] * inv, st.acc[1][nb][i] * inv);
+                        o.y = pack_bf16x2(st.acc[2][nb][i] * inv, st.acc[3][nb][i] * inv);
+                        o.z = pack_bf16x2(st.acc[4][nb][i] * inv, st.acc[5][nb][i] * inv);
+                        o.w = pack_bf16x2(st.acc[6][nb][i] * inv, st.acc[7][nb][i] * inv);
+                        *reinterpret_cast<u32x4 *>(reinterpret_cast<uint16_t *>(p.out) + off + 8 * i) = o;
+                    } else {
+                        float *o = reinterpret_cast<float *>(p.out) + off + 8 * i;
+                        *reinterpret_cast<f32x4 *>(o) = f32x4{st.acc[0][nb][i], st.acc[1][nb][i],
+                                                              st.acc[2][nb][i], st.acc[3][nb][i]} * inv;
+                        *reinterpret_cast<f32x4 *>(o + 4) = f32x4{st.acc[4][nb][i], st.acc[5][nb][i],
+                                                                  st.acc[6][nb][i], st.acc[7][nb][i]} * inv;
+                    }
+                }
+                if (j == 0 && p.lse != nullptr)
+                    p.lse[lse_index(p, b, h, r)] = lse2 * 0.69314718055994531f;
+            } else {
+                float *o = pl.part_o + (slot * pl.rows + r) * (int64_t)p.D + 32 * j;
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    *reinterpret_cast<f32x4 *>(o + 8 * i) = f32x4{st.acc[0][nb][i], st.acc[1][nb][i],
+                                                                  st.acc[2][nb][i], st.acc[3][nb][i]} * inv;
+                    *reinterpret_cast<f32x4 *>(o + 8 * i + 4) = f32x4{st.acc[4][nb][i], st.acc[5][nb][i],
+                                                                      st.acc[6][nb][i], st.acc[7][nb][i]} * inv;
+                }
+                if (j == 0) pl.part_lse[slot * pl.rows + r] = lse2;
+            }
+        }
+        pos += t1 - tile;
+        ++seg;
+        tile = 0;
+    }
+}
+
+template <bool FP8, int NB>
+static hipError_t launch_nb(const Problem &p, const Plan &pl, hipStream_t st) {
+    const dim3 grid((pl.workers + kMfmaWavesPerWG - 1) / kMfmaWavesPerWG), block(64 * kMfmaWavesPerWG);
+    if (p.draft)
+        hipLaunchKernelGGL((mfma_partial_kernel<FP8, NB, MODE_DRAFT>), grid, block, 0, st, p, pl);
+    else if (p.kv.page_size > 0)
+        hipLaunchKernelGGL((mfma_partial_kernel<FP8, NB, MODE_PAGED>), grid, block, 0, st, p, pl);
+    else
+        hipLaunchKernelGGL((mfma_partial_kernel<FP8, NB, MODE_CONTIG>), grid, block, 0, st, p, pl);
+    return hipGetLastError();
+}
+
+template <bool FP8>
+static hipError_t launch_fp(const Problem &p, const Plan &pl, int nb, hipStream_t st) {
+    switch (nb) {
+    case 1: return launch_nb<FP8, 1>(p, pl, st);
+    case 2: return launch_nb<FP8, 2>(p, pl, st);
+    case 3: return launch_nb<FP8, 3>(p, pl, st);
+    case 4: return launch_nb<FP8, 4>(p, pl, st);
+    case 5: return launch_nb<FP8, 5>(p, pl, st);
+    default: return hipErrorInvalidValue;
+    }
+}
+
+hipError_t launch_mfma_partial(const Problem &p, const Plan &pl, int nb, hipStream_t st) {
+    if (p.kv_dtype == SPIRE_FP8_E4M3FN) return launch_fp<true>(p, pl, nb, st);
+    return launch_fp<false>(p, pl, nb, st);
+}
+
+}  // namespace spire

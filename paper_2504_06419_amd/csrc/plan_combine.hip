@@ -1,0 +1,164 @@
+// plan_combine.hip -- work partition (plan) and split-segment merge (combine).
+//
+// The plan reads the per-sequence lengths on the device, clamps them to what
+// the cache descriptors can address, cuts every sequence into key tiles and
+// assigns each worker an equal share of all tiles (see spire_internal.h).  It
+// runs as one workgroup; everything it produces stays in the caller's
+// workspace.
+//
+// The combine merges the partial results of a segment that several workers
+// shared: with partials (o_p, lse_p) in base 2,
+//   M = max_p lse_p,  w_p = 2^(lse_p - M),  out = sum_p w_p o_p / sum_p w_p,
+//   lse = (M + log2 sum_p w_p) * ln 2,
+// the log-sum-exp identity that makes attention over a union of disjoint key
+// sets equal to a weighted merge of attention over each set.
+#include "spire_internal.h"
+
+namespace spire {
+
+constexpr int kPlanThreads = 1024;
+constexpr int kPlanMaxB = 8192;
+
+__device__ __forceinline__ int effective_keys(const Problem &p, int b) {
+    int n = p.lens[b];
+    if (!p.draft) {
+        int64_t cap = p.kv.page_size > 0 ? (int64_t)p.kv.max_blocks * p.kv.page_size
+                                         : (int64_t)p.kv.capacity;
+        if (cap > INT32_MAX) cap = INT32_MAX;
+        n = n < 0 ? 0 : (n > cap ? (int)cap : n);
+    } else {
+        const int m = n < 0 ? 0 : n;
+        const int ns = m < p.S ? m : p.S;
+        int nr = m - p.S;
+        nr = nr < 0 ? 0 : (nr > p.W ? p.W : nr);
+        n = ns + nr;
+    }
+    return n;
+}
+
+__global__ __launch_bounds__(kPlanThreads) void plan_kernel(Problem p, Plan pl) {
+    __shared__ int32_t prefix[kPlanMaxB + 1];
+    __shared__ int32_t sums[kPlanThreads];
+    const int tid = threadIdx.x;
+    const int B = p.B;
+    const int per = (B + kPlanThreads - 1) / kPlanThreads;
+    const int b0 = tid * per;
+    const int b1 = b0 + per < B ? b0 + per : B;
+    int local = 0;
+    for (int b = b0; b < b1; ++b) {
+        const int n = effective_keys(p, b);
+        pl.nkeys[b] = n;
+        const int tiles = n > 0 ? (n + pl.tile - 1) / pl.tile : 1;
+        prefix[b] = tiles;  // temporarily the tile count
+        local += tiles;
+    }
+    sums[tid] = local;
+    __syncthreads();
+    for (int off = 1; off < kPlanThreads; off <<= 1) {  // inclusive scan
+        const int v = tid >= off ? sums[tid - off] : 0;
+        __syncthreads();
+        sums[tid] += v;
+        __syncthreads();
+    }
+    int run = sums[tid] - local;
+    for (int b = b0; b < b1; ++b) {
+        const int tiles = prefix[b];
+        prefix[b] = run;
+        pl.prefix[b] = run;
+        run += tiles;
+    }
+    if (tid == kPlanThreads - 1) {
+        prefix[B] = sums[kPlanThreads - 1];
+        pl.prefix[B] = sums[kPlanThreads - 1];
+    }
+    __syncthreads();
+    const int64_t T = (int64_t)prefix[B] * pl.units;
+    for (int w = tid; w < pl.workers; w += kPlanThreads) {
+        const int64_t x = worker_begin(w, T, pl.workers);
+        if (x >= worker_begin(w + 1, T, pl.workers)) {  // empty range
+            pl.wstart[2 * w] = -1;
+            pl.wstart[2 * w + 1] = 0;
+            continue;
+        }
+        int lo = 0, hi = B - 1;  // last b with units * prefix[b] <= x
+        while (lo < hi) {
+            const int mid = (lo + hi + 1) >> 1;
+            if ((int64_t)prefix[mid] * pl.units <= x) lo = mid; else hi = mid - 1;
+        }
+        const int tiles = prefix[lo + 1] - prefix[lo];
+        const int64_t rel = x - (int64_t)prefix[lo] * pl.units;
+        pl.wstart[2 * w] = lo * pl.units + (int)(rel / tiles);
+        pl.wstart[2 * w + 1] = (int)(rel % tiles);
+    }
+}
+
+hipError_t launch_plan(const Problem &p, const Plan &pl, hipStream_t st) {
+    if (p.B > kPlanMaxB) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(kPlanThreads), 0, st, p, pl);
+    return hipGetLastError();
+}
+
+// One workgroup per segment; segments that one worker covered return at once.
+__global__ __launch_bounds__(256) void combine_kernel(Problem p, Plan pl) {
+    const int seg = blockIdx.x;
+    const int b = seg / pl.units, u = seg - (seg / pl.units) * pl.units;
+    const int tiles = pl.prefix[b + 1] - pl.prefix[b];
+    const int64_t T = (int64_t)pl.prefix[p.B] * pl.units;
+    const int64_t start = (int64_t)pl.prefix[b] * pl.units + (int64_t)u * tiles;
+    const int64_t wlo = worker_of(start, T, pl.workers);
+    const int64_t whi = worker_of(start + tiles - 1, T, pl.workers);
+    if (wlo == whi) return;
+
+    // rows of this unit
+    const int nrb = pl.units / p.Hkv;  // row blocks per KV head
+    const int h = u / nrb;
+    const int r0 = (u - h * nrb) * pl.rows;
+    const int nrows = p.R - r0 < pl.rows ? p.R - r0 : pl.rows;
+    const int d4n = p.D >> 2;
+    const int64_t begin_lo = worker_begin(wlo, T, pl.workers);
+
+    for (int idx = threadIdx.x; idx < nrows * d4n; idx += blockDim.x) {
+        const int r = idx / d4n, d4 = idx - (idx / d4n) * d4n;
+        float M = -INFINITY;
+        for (int64_t w = wlo; w <= whi; ++w) {
+            const int64_t slot = 2 * w + ((w == wlo && begin_lo < start) ? 1 : 0);
+            M = fmaxf(M, pl.part_lse[slot * pl.rows + r]);
+        }
+        float L = 0.f;
+        float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (M != -INFINITY) {
+            for (int64_t w = wlo; w <= whi; ++w) {
+                const int64_t slot = 2 * w + ((w == wlo && begin_lo < start) ? 1 : 0);
+                const float lp = pl.part_lse[slot * pl.rows + r];
+                const float wgt = lp == -INFINITY ? 0.f : exp2f(lp - M);
+                const float4 o = *reinterpret_cast<const float4 *>(
+                    pl.part_o + (slot * pl.rows + r) * (int64_t)p.D + 4 * d4);
+                L += wgt;
+                acc.x += wgt * o.x; acc.y += wgt * o.y; acc.z += wgt * o.z; acc.w += wgt * o.w;
+            }
+        }
+        const float inv = L > 0.f ? 1.f / L : 0.f;
+        const int64_t off = row_offset(p, b, h, r0 + r) + 4 * d4;
+        if (p.out_dtype == SPIRE_BF16) {
+            uint16_t *o = reinterpret_cast<uint16_t *>(p.out) + off;
+            const uint32_t lo = f32_to_bf16_rne(acc.x * inv) | ((uint32_t)f32_to_bf16_rne(acc.y * inv) << 16);
+            const uint32_t hi = f32_to_bf16_rne(acc.z * inv) | ((uint32_t)f32_to_bf16_rne(acc.w * inv) << 16);
+            *reinterpret_cast<uint2 *>(o) = make_uint2(lo, hi);
+        } else {
+            *reinterpret_cast<float4 *>(reinterpret_cast<float *>(p.out) + off) =
+                make_float4(acc.x * inv, acc.y * inv, acc.z * inv, acc.w * inv);
+        }
+        if (d4 == 0 && p.lse != nullptr)
+            p.lse[lse_index(p, b, h, r0 + r)] = L > 0.f ? (M + log2f(L)) * 0.69314718055994531f
+                                                         : -INFINITY;
+    }
+}
+
+hipError_t launch_combine(const Problem &p, const Plan &pl, hipStream_t st) {
+    const int64_t segs = (int64_t)p.B * pl.units;
+    if (segs == 0) return hipSuccess;
+    hipLaunchKernelGGL(combine_kernel, dim3((unsigned)segs), dim3(256), 0, st, p, pl);
+    return hipGetLastError();
+}
+
+}  // namespace spire

@@ -1,0 +1,386 @@
+// spire_abi.hip -- host implementation of the C ABI in include/spire.h.
+//
+// Validates arguments, lays out the caller's workspace, picks the kernel
+// family (matrix-core for bf16/fp8 K/V with head_dim 128, generic otherwise)
+// and enqueues plan -> partial attention -> combine on the caller's stream.
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <mutex>
+#include <vector>
+
+#include "spire_internal.h"
+
+using namespace spire;
+
+namespace {
+
+thread_local char g_err[512] = "";
+int g_variant = 0;
+
+spire_status fail(spire_status s, const char *fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_err, sizeof g_err, fmt, ap);
+    va_end(ap);
+    return s;
+}
+
+// ---- device properties ------------------------------------------------------
+constexpr int kMaxDevices = 64;
+int g_cus[kMaxDevices] = {0};
+std::mutex g_dev_mu;
+
+int device_cus(int *cus_out) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return -1;
+    std::lock_guard<std::mutex> lock(g_dev_mu);
+    if (g_cus[dev] == 0) {
+        int n = 0;
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+            return -1;
+        g_cus[dev] = n;
+    }
+    *cus_out = g_cus[dev];
+    return 0;
+}
+
+// ---- workspace layout -------------------------------------------------------
+struct Layout {
+    size_t nkeys, prefix, wstart, part_lse, part_o, total;
+};
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+Layout layout(int64_t B, int64_t rows, int64_t D, int64_t workers) {
+    Layout L;
+    size_t off = 0;
+    L.nkeys = off; off = align256(off + 4 * (size_t)B);
+    L.prefix = off; off = align256(off + 4 * (size_t)(B + 1));
+    L.wstart = off; off = align256(off + 8 * (size_t)workers);
+    L.part_lse = off; off = align256(off + 4 * (size_t)(2 * workers * rows));
+    L.part_o = off; off = align256(off + 4 * (size_t)(2 * workers * rows * D));
+    L.total = off;
+    return L;
+}
+
+int mfma_workers(int cus) { return cus * kMfmaWavesPerWG; }
+int generic_workers(int cus) { return cus * kMaxWorkersPerCU; }
+
+size_t workspace_bytes_for(int B, int R, int D) {
+    int cus = 0;
+    if (device_cus(&cus) != 0) return 0;
+    const Layout a = layout(B, R, D, mfma_workers(cus));
+    const Layout b = layout(B, kGenericRowBlock, D, generic_workers(cus));
+    return a.total > b.total ? a.total : b.total;
+}
+
+// ---- timing -----------------------------------------------------------------
+constexpr int kTimingSlots = 4096;
+struct TimingRec {
+    hipEvent_t a, b;
+    int id;
+};
+std::vector<TimingRec> g_ev;
+int g_ev_next = 0, g_ev_count = 0;
+bool g_timing = false;
+
+hipError_t timed_launch(int id, hipStream_t st, hipError_t (*fn)(const Problem &, const Plan &, hipStream_t),
+                        const Problem &p, const Plan &pl) {
+    if (!g_timing) return fn(p, pl, st);
+    TimingRec &r = g_ev[g_ev_next];
+    r.id = id;
+    hipError_t e = hipEventRecord(r.a, st);
+    if (e != hipSuccess) return e;
+    e = fn(p, pl, st);
+    if (e != hipSuccess) return e;
+    e = hipEventRecord(r.b, st);
+    g_ev_next = (g_ev_next + 1) % kTimingSlots;
+    if (g_ev_count < kTimingSlots) ++g_ev_count;
+    return e;
+}
+
+// ---- argument checks --------------------------------------------------------
+bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
+
+int elem_size(int dt) {
+    switch (dt) {
+    case SPIRE_F32: return 4;
+    case SPIRE_BF16: return 2;
+    case SPIRE_FP8_E4M3FN: return 1;
+    default: return 0;
+    }
+}
+
+spire_status check_kv(const spire_kv *kv, const char *name, int D, int Hkv, bool allow_paged) {
+    if (kv == nullptr) return fail(SPIRE_ERR_INVALID_ARG, "%s: descriptor is NULL", name);
+    if (kv->k == nullptr || kv->v == nullptr) return fail(SPIRE_ERR_INVALID_ARG, "%s: k or v is NULL", name);
+    const int es = elem_size(kv->dtype);
+    if (es == 0) return fail(SPIRE_ERR_INVALID_ARG, "%s: unknown dtype %d", name, kv->dtype);
+    if (kv->reserved != 0) return fail(SPIRE_ERR_INVALID_ARG, "%s: reserved field must be 0", name);
+    if (kv->s_blk < 0 || kv->s_head < 0 || kv->s_tok < 0)
+        return fail(SPIRE_ERR_INVALID_ARG, "%s: negative stride", name);
+    if (kv->dtype == SPIRE_FP8_E4M3FN && (kv->k_scale == nullptr || kv->v_scale == nullptr))
+        return fail(SPIRE_ERR_INVALID_ARG, "%s: fp8 storage needs k_scale and v_scale", name);
+    if (kv->page_size < 0) return fail(SPIRE_ERR_INVALID_ARG, "%s: negative page_size", name);
+    if (kv->page_size > 0) {
+        if (!allow_paged) return fail(SPIRE_ERR_UNSUPPORTED, "%s: paged storage not supported here", name);
+        if (kv->block_table == nullptr || kv->max_blocks <= 0 || kv->num_blocks <= 0)
+            return fail(SPIRE_ERR_INVALID_ARG, "%s: paged view needs block_table, max_blocks > 0, num_blocks > 0", name);
+    } else {
+        if (kv->capacity < 0) return fail(SPIRE_ERR_INVALID_ARG, "%s: negative capacity", name);
+    }
+    (void)D; (void)Hkv;
+    return SPIRE_OK;
+}
+
+KvDev to_dev(const spire_kv *kv) {
+    KvDev d;
+    d.k = static_cast<const uint8_t *>(kv->k);
+    d.v = static_cast<const uint8_t *>(kv->v);
+    d.block_table = kv->block_table;
+    d.k_scale = kv->k_scale;
+    d.v_scale = kv->v_scale;
+    d.s_blk = kv->s_blk;
+    d.s_head = kv->s_head;
+    d.s_tok = kv->s_tok;
+    d.elem = elem_size(kv->dtype);
+    d.page_size = kv->page_size;
+    d.max_blocks = kv->max_blocks;
+    d.num_blocks = kv->num_blocks;
+    d.capacity = kv->capacity;
+    return d;
+}
+
+bool rows_aligned(const spire_kv *kv) {
+    const int es = elem_size(kv->dtype);
+    return aligned16(kv->k) && aligned16(kv->v) && (kv->s_blk * es) % 16 == 0 &&
+           (kv->s_head * es) % 16 == 0 && (kv->s_tok * es) % 16 == 0;
+}
+
+spire_status common_checks(const void *q, int q_dtype, int B, int Hq, int Hkv, int D, int k,
+                           const void *out, int out_dtype, const void *workspace) {
+    if (B < 0) return fail(SPIRE_ERR_INVALID_ARG, "B must be >= 0 (got %d)", B);
+    if (Hkv <= 0 || Hq <= 0 || Hq % Hkv != 0)
+        return fail(SPIRE_ERR_INVALID_ARG, "need Hkv >= 1 and Hq %% Hkv == 0 (Hq=%d, Hkv=%d)", Hq, Hkv);
+    if (D != 64 && D != 128) return fail(SPIRE_ERR_UNSUPPORTED, "head_dim must be 64 or 128 (got %d)", D);
+    if (k < 0 || k > 15) return fail(SPIRE_ERR_UNSUPPORTED, "k must be in [0, 15] (got %d)", k);
+    if ((int64_t)(k + 1) * (Hq / Hkv) > kMaxRows)
+        return fail(SPIRE_ERR_UNSUPPORTED, "(k+1)*Hq/Hkv = %d exceeds %d", (k + 1) * (Hq / Hkv), kMaxRows);
+    if (q_dtype != SPIRE_F32 && q_dtype != SPIRE_BF16)
+        return fail(SPIRE_ERR_UNSUPPORTED, "q_dtype must be F32 or BF16");
+    if (out_dtype != SPIRE_F32 && out_dtype != SPIRE_BF16)
+        return fail(SPIRE_ERR_UNSUPPORTED, "out_dtype must be F32 or BF16");
+    if (B > 0 && (q == nullptr || out == nullptr)) return fail(SPIRE_ERR_INVALID_ARG, "q or out is NULL");
+    if (B > 0 && workspace == nullptr) return fail(SPIRE_ERR_WORKSPACE, "workspace is NULL");
+    if (B > 8192) return fail(SPIRE_ERR_UNSUPPORTED, "B must be <= 8192 (got %d)", B);
+    if (!aligned16(q) || !aligned16(out)) return fail(SPIRE_ERR_INVALID_ARG, "q and out must be 16-byte aligned");
+    if (((uintptr_t)workspace & 255u) != 0) return fail(SPIRE_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+    return SPIRE_OK;
+}
+
+spire_status run(Problem &p, bool use_mfma, void *workspace, size_t ws_bytes, hipStream_t stream,
+                 int partial_id) {
+    int cus = 0;
+    if (device_cus(&cus) != 0) return fail(SPIRE_ERR_HIP, "cannot query the current HIP device");
+    const bool mf = use_mfma && g_variant == 0;
+    Plan pl;
+    pl.tile = mf ? kMfmaTile : kGenericTile;
+    const int nrb = mf ? 1 : (p.R + kGenericRowBlock - 1) / kGenericRowBlock;
+    pl.units = p.Hkv * nrb;
+    pl.rows = mf ? p.R : kGenericRowBlock;
+    pl.workers = mf ? mfma_workers(cus) : generic_workers(cus);
+    const Layout L = layout(p.B, pl.rows, p.D, pl.workers);
+    if (ws_bytes < L.total)
+        return fail(SPIRE_ERR_WORKSPACE, "workspace has %zu bytes, needs %zu", ws_bytes, L.total);
+    char *ws = static_cast<char *>(workspace);
+    pl.nkeys = reinterpret_cast<int32_t *>(ws + L.nkeys);
+    pl.prefix = reinterpret_cast<int32_t *>(ws + L.prefix);
+    pl.wstart = reinterpret_cast<int32_t *>(ws + L.wstart);
+    pl.part_lse = reinterpret_cast<float *>(ws + L.part_lse);
+    pl.part_o = reinterpret_cast<float *>(ws + L.part_o);
+
+    hipError_t e = timed_launch(0, stream, launch_plan, p, pl);
+    if (e != hipSuccess) return fail(SPIRE_ERR_HIP, "plan launch: %s", hipGetErrorString(e));
+    if (mf) {
+        const int nb = (p.R + 15) / 16;
+        auto fn = [](const Problem &pp, const Plan &pp2, hipStream_t s) {
+            return launch_mfma_partial(pp, pp2, (pp.R + 15) / 16, s);
+        };
+        (void)nb;
+        e = timed_launch(partial_id, stream, fn, p, pl);
+    } else {
+        e = timed_launch(partial_id, stream, launch_generic_partial, p, pl);
+    }
+    if (e != hipSuccess) return fail(SPIRE_ERR_HIP, "attention launch: %s", hipGetErrorString(e));
+    e = timed_launch(3, stream, launch_combine, p, pl);
+    if (e != hipSuccess) return fail(SPIRE_ERR_HIP, "combine launch: %s", hipGetErrorString(e));
+    return SPIRE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t spire_version(void) { return SPIRE_VERSION; }
+
+const char *spire_status_string(spire_status s) {
+    switch (s) {
+    case SPIRE_OK: return "SPIRE_OK";
+    case SPIRE_ERR_INVALID_ARG: return "SPIRE_ERR_INVALID_ARG";
+    case SPIRE_ERR_UNSUPPORTED: return "SPIRE_ERR_UNSUPPORTED";
+    case SPIRE_ERR_WORKSPACE: return "SPIRE_ERR_WORKSPACE";
+    case SPIRE_ERR_HIP: return "SPIRE_ERR_HIP";
+    default: return "SPIRE_ERR_UNKNOWN";
+    }
+}
+
+const char *spire_last_error(void) { return g_err; }
+
+spire_status spire_set_kernel_variant(int32_t variant) {
+    if (variant != 0 && variant != 1) return fail(SPIRE_ERR_INVALID_ARG, "variant must be 0 or 1");
+    g_variant = variant;
+    return SPIRE_OK;
+}
+
+size_t spire_verify_workspace_size(int32_t B, int32_t Hq, int32_t Hkv, int32_t D, int32_t k) {
+    if (B < 0 || Hkv <= 0 || Hq <= 0 || Hq % Hkv != 0 || D <= 0 || k < 0) return 0;
+    return workspace_bytes_for(B, (k + 1) * (Hq / Hkv), D);
+}
+
+size_t spire_draft_workspace_size(int32_t B, int32_t Hq, int32_t Hkv, int32_t D) {
+    if (B < 0 || Hkv <= 0 || Hq <= 0 || Hq % Hkv != 0 || D <= 0) return 0;
+    return workspace_bytes_for(B, Hq / Hkv, D);
+}
+
+spire_status spire_verify_attn(const void *q, int32_t q_dtype, const spire_kv *kv,
+                               const int32_t *kv_lens, int32_t B, int32_t Hq, int32_t Hkv,
+                               int32_t D, int32_t k, float sm_scale, void *out,
+                               int32_t out_dtype, float *lse, void *workspace,
+                               size_t workspace_bytes, hipStream_t stream) {
+    g_err[0] = '\0';
+    spire_status s = common_checks(q, q_dtype, B, Hq, Hkv, D, k, out, out_dtype, workspace);
+    if (s != SPIRE_OK) return s;
+    s = check_kv(kv, "kv", D, Hkv, true);
+    if (s != SPIRE_OK) return s;
+    if (B > 0 && kv_lens == nullptr) return fail(SPIRE_ERR_INVALID_ARG, "kv_lens is NULL");
+    if (kv->page_size == 0 && kv->capacity <= 0 && B > 0)
+        return fail(SPIRE_ERR_INVALID_ARG, "contiguous kv needs capacity > 0");
+    if (B == 0) return SPIRE_OK;
+
+    Problem p;
+    memset(&p, 0, sizeof p);
+    p.draft = 0;
+    p.B = B; p.Hq = Hq; p.Hkv = Hkv; p.D = D; p.k = k;
+    p.g = Hq / Hkv;
+    p.R = (k + 1) * p.g;
+    p.sm_scale_log2 = sm_scale * 1.4426950408889634f;
+    p.q = static_cast<const uint8_t *>(q);
+    p.q_dtype = q_dtype;
+    p.kv_dtype = kv->dtype;
+    p.lens = kv_lens;
+    p.kv = to_dev(kv);
+    p.out = out;
+    p.out_dtype = out_dtype;
+    p.lse = lse;
+
+    const bool layout_ok = kv->page_size > 0 ? (kv->page_size % 16 == 0)
+                                             : (kv->capacity >= 16 && kv->capacity % 16 == 0);
+    const bool mfma = (kv->dtype == SPIRE_BF16 || kv->dtype == SPIRE_FP8_E4M3FN) &&
+                      q_dtype == SPIRE_BF16 && D == 128 && p.R <= 80 && layout_ok && rows_aligned(kv);
+    return run(p, mfma, workspace, workspace_bytes, stream, 1);
+}
+
+spire_status spire_draft_sparse_attn(const void *q, int32_t q_dtype, const spire_kv *sink,
+                                     const spire_kv *ring, const int32_t *seq_lens,
+                                     const int32_t *ring_offset, int32_t B, int32_t Hq,
+                                     int32_t Hkv, int32_t D, int32_t S, int32_t W, float sm_scale,
+                                     void *out, int32_t out_dtype, float *lse, void *workspace,
+                                     size_t workspace_bytes, hipStream_t stream) {
+    g_err[0] = '\0';
+    spire_status s = common_checks(q, q_dtype, B, Hq, Hkv, D, 0, out, out_dtype, workspace);
+    if (s != SPIRE_OK) return s;
+    if (S < 0 || W < 0 || (int64_t)S + W < 1)
+        return fail(SPIRE_ERR_INVALID_ARG, "need S >= 0, W >= 0, S + W >= 1 (S=%d, W=%d)", S, W);
+    s = check_kv(sink, "sink", D, Hkv, false);
+    if (s != SPIRE_OK) return s;
+    s = check_kv(ring, "ring", D, Hkv, false);
+    if (s != SPIRE_OK) return s;
+    if (sink->dtype != ring->dtype) return fail(SPIRE_ERR_INVALID_ARG, "sink and ring dtypes differ");
+    if (sink->capacity < S) return fail(SPIRE_ERR_INVALID_ARG, "sink capacity %d < S = %d", sink->capacity, S);
+    if (ring->capacity < W) return fail(SPIRE_ERR_INVALID_ARG, "ring capacity %d < W = %d", ring->capacity, W);
+    if (B > 0 && (seq_lens == nullptr || ring_offset == nullptr))
+        return fail(SPIRE_ERR_INVALID_ARG, "seq_lens or ring_offset is NULL");
+    if (B == 0) return SPIRE_OK;
+
+    Problem p;
+    memset(&p, 0, sizeof p);
+    p.draft = 1;
+    p.B = B; p.Hq = Hq; p.Hkv = Hkv; p.D = D; p.k = 0;
+    p.g = Hq / Hkv;
+    p.R = p.g;
+    p.S = S; p.W = W;
+    p.sm_scale_log2 = sm_scale * 1.4426950408889634f;
+    p.q = static_cast<const uint8_t *>(q);
+    p.q_dtype = q_dtype;
+    p.kv_dtype = ring->dtype;
+    p.lens = seq_lens;
+    p.ring_offset = ring_offset;
+    p.kv = to_dev(ring);
+    p.sink = to_dev(sink);
+    p.out = out;
+    p.out_dtype = out_dtype;
+    p.lse = lse;
+
+    const bool same_scales = ring->dtype != SPIRE_FP8_E4M3FN ||
+                             (ring->k_scale == sink->k_scale && ring->v_scale == sink->v_scale);
+    const bool mfma = (ring->dtype == SPIRE_BF16 || ring->dtype == SPIRE_FP8_E4M3FN) &&
+                      q_dtype == SPIRE_BF16 && D == 128 && p.R <= 80 && same_scales &&
+                      rows_aligned(ring) && rows_aligned(sink);
+    return run(p, mfma, workspace, workspace_bytes, stream, 2);
+}
+
+spire_status spire_timing_enable(int32_t on) {
+    if (on) {
+        if (g_timing) return SPIRE_OK;
+        g_ev.resize(kTimingSlots);
+        for (auto &r : g_ev) {
+            if (hipEventCreate(&r.a) != hipSuccess || hipEventCreate(&r.b) != hipSuccess)
+                return fail(SPIRE_ERR_HIP, "hipEventCreate failed");
+        }
+        g_ev_next = 0;
+        g_ev_count = 0;
+        g_timing = true;
+    } else {
+        if (!g_timing) return SPIRE_OK;
+        for (auto &r : g_ev) {
+            (void)hipEventDestroy(r.a);
+            (void)hipEventDestroy(r.b);
+        }
+        g_ev.clear();
+        g_timing = false;
+    }
+    return SPIRE_OK;
+}
+
+int32_t spire_timing_collect(int32_t *kernel_ids, float *ms, int32_t max) {
+    if (!g_timing) return 0;
+    int written = 0;
+    const int first = (g_ev_next - g_ev_count + kTimingSlots) % kTimingSlots;
+    for (int i = 0; i < g_ev_count; ++i) {
+        TimingRec &r = g_ev[(first + i) % kTimingSlots];
+        if (hipEventSynchronize(r.b) != hipSuccess) continue;
+        float t = 0.f;
+        if (hipEventElapsedTime(&t, r.a, r.b) != hipSuccess) continue;
+        if (written < max) {
+            if (kernel_ids) kernel_ids[written] = r.id;
+            if (ms) ms[written] = t;
+            ++written;
+        }
+    }
+    g_ev_count = 0;
+    return written;
+}
+
+}  // extern "C"

@@ -1,0 +1,128 @@
+// spire_internal.h -- shared declarations of the HIP library (not part of the ABI).
+//
+// Work partition used by every attention kernel ("stream-K" over keys):
+//   * the keys of sequence b are cut into tiles of `tile` keys; a sequence
+//     with no key still owns one (empty) tile so that its rows get written;
+//   * a segment is one (sequence b, unit u) pair, where a unit is one KV head
+//     (matrix-core kernels) or one KV head x 16-row block (generic kernel);
+//     segment s = b * units + u owns tiles_b consecutive positions;
+//   * the flattened positions [0, T), T = units * sum_b tiles_b, are split into
+//     `workers` contiguous ranges of equal length: worker w owns
+//     [w*T/workers, (w+1)*T/workers);
+//   * a worker that covers a whole segment writes the final rows; otherwise it
+//     writes a partial (normalised output + base-2 log-sum-exp) into slot 2w
+//     (the segment it starts in) or 2w+1 (the segment it ends in), and the
+//     combine kernel merges the partials of each split segment.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/spire.h"
+
+namespace spire {
+
+constexpr int kMaxRows = 128;          // (k+1) * Hq/Hkv
+constexpr int kGenericRowBlock = 16;   // rows per unit in the generic kernel
+constexpr int kMaxWorkersPerCU = 8;
+
+// Device-side description of one K/V view (byte pointers, element strides).
+struct KvDev {
+    const uint8_t *k;
+    const uint8_t *v;
+    const int32_t *block_table;
+    const float *k_scale;
+    const float *v_scale;
+    int64_t s_blk, s_head, s_tok;  // elements
+    int32_t elem;                  // bytes per element
+    int32_t page_size;             // 0 = contiguous
+    int32_t max_blocks;
+    int32_t num_blocks;
+    int32_t capacity;              // contiguous: rows per sequence
+};
+
+// Everything an attention kernel needs to know about the request.
+struct Problem {
+    int32_t draft;          // 0: verify, 1: draft step
+    int32_t B, Hq, Hkv, D;
+    int32_t k;              // verify: draft tokens; draft: 0
+    int32_t g;              // Hq / Hkv
+    int32_t R;              // rows per KV head: (k+1) * g
+    int32_t S, W;           // draft sinks / window
+    float sm_scale_log2;    // sm_scale * log2(e)
+    const uint8_t *q;
+    int32_t q_dtype;        // SPIRE_F32 / SPIRE_BF16
+    int32_t kv_dtype;
+    const int32_t *lens;         // verify: kv_lens; draft: seq_lens
+    const int32_t *ring_offset;  // draft only
+    KvDev kv;               // verify cache, or the draft ring
+    KvDev sink;             // draft sinks
+    void *out;
+    int32_t out_dtype;
+    float *lse;
+};
+
+// Partition state in the workspace.
+struct Plan {
+    int32_t *nkeys;     // [B]   keys of each sequence after clamping
+    int32_t *prefix;    // [B+1] exclusive prefix sum of tiles per sequence
+    int32_t *wstart;    // [2*workers] (segment, tile) where each worker starts
+    float *part_lse;    // [2*workers, rows]       base-2 log-sum-exp of a partial
+    float *part_o;      // [2*workers, rows, D]    normalised partial output
+    int32_t tile;       // keys per tile
+    int32_t units;      // segments per sequence
+    int32_t rows;       // rows per segment (partials stride)
+    int32_t workers;
+};
+
+__device__ __forceinline__ int64_t worker_begin(int64_t w, int64_t T, int64_t workers) {
+    return (w * T) / workers;
+}
+// the worker whose range contains flattened position x (0 <= x < T)
+__device__ __forceinline__ int64_t worker_of(int64_t x, int64_t T, int64_t workers) {
+    return ((x + 1) * workers - 1) / T;
+}
+
+// Row r of KV head h (r in [0, R)) -> element offset of its query/output row
+// in [B, k+1, Hq, D]: rows are ordered (draft index i, head in group hg).
+__device__ __forceinline__ int64_t row_offset(const Problem &p, int b, int h, int r) {
+    const int i = r / p.g, hg = r - (r / p.g) * p.g;
+    return (((int64_t)b * (p.k + 1) + i) * p.Hq + (int64_t)h * p.g + hg) * p.D;
+}
+__device__ __forceinline__ int64_t lse_index(const Problem &p, int b, int h, int r) {
+    const int i = r / p.g, hg = r - (r / p.g) * p.g;
+    return ((int64_t)b * (p.k + 1) + i) * p.Hq + (int64_t)h * p.g + hg;
+}
+
+// Keys visible to row r of a sequence holding n keys: verify rows see
+// [0, n - k + i); draft rows see everything the segment holds.
+__device__ __forceinline__ int visible_limit(const Problem &p, int n, int r) {
+    if (p.draft) return n;
+    int i = r / p.g;
+    if (i > p.k) i = p.k;
+    return n - p.k + i;
+}
+
+__device__ __forceinline__ float bf16_to_f32(uint16_t x) {
+    return __uint_as_float((uint32_t)x << 16);
+}
+// round-to-nearest-even fp32 -> bf16 bits (NaN kept quiet)
+__device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+
+// ---- host-side launchers (one per kernel family) ---------------------------
+hipError_t launch_plan(const Problem &p, const Plan &pl, hipStream_t st);
+hipError_t launch_mfma_partial(const Problem &p, const Plan &pl, int nb, hipStream_t st);
+hipError_t launch_generic_partial(const Problem &p, const Plan &pl, hipStream_t st);
+hipError_t launch_combine(const Problem &p, const Plan &pl, hipStream_t st);
+
+// MFMA kernel tile size (keys) and its worker count per CU.
+constexpr int kMfmaTile = 32;
+constexpr int kMfmaWavesPerWG = 4;
+constexpr int kGenericTile = 64;
+
+}  // namespace spire

@@ -1,0 +1,195 @@
+"""Thin Python binding of libspire.so (argument marshalling only).
+
+Each function takes torch tensors that already live on the current HIP device,
+fills the C descriptors of include/spire.h with their device pointers and
+strides, and calls the entry point of the same name on torch's current stream.
+All arithmetic happens in the library's HIP kernels; there is no fallback: if
+the library is missing or a call fails, an exception is raised.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+from typing import Optional
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libspire.so")
+
+F32, BF16, FP8 = 0, 1, 2
+_DT = {torch.float32: F32, torch.bfloat16: BF16, torch.float8_e4m3fn: FP8}
+STATUS = {0: "SPIRE_OK", 1: "SPIRE_ERR_INVALID_ARG", 2: "SPIRE_ERR_UNSUPPORTED",
+          3: "SPIRE_ERR_WORKSPACE", 4: "SPIRE_ERR_HIP"}
+
+# exported symbols, in the order include/spire.h declares them
+SYMBOLS = ["spire_verify_workspace_size", "spire_verify_attn", "spire_draft_workspace_size",
+           "spire_draft_sparse_attn", "spire_status_string", "spire_last_error", "spire_version",
+           "spire_set_kernel_variant", "spire_timing_enable", "spire_timing_collect"]
+
+KERNEL_IDS = {0: "plan", 1: "verify_partial", 2: "draft_partial", 3: "combine"}
+
+
+class SpireError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{STATUS.get(status, status)}: {msg}")
+        self.status = status
+
+
+class KV(C.Structure):
+    """struct spire_kv"""
+    _fields_ = [("k", C.c_void_p), ("v", C.c_void_p), ("block_table", C.c_void_p),
+                ("k_scale", C.c_void_p), ("v_scale", C.c_void_p),
+                ("s_blk", C.c_int64), ("s_head", C.c_int64), ("s_tok", C.c_int64),
+                ("dtype", C.c_int32), ("page_size", C.c_int32), ("max_blocks", C.c_int32),
+                ("num_blocks", C.c_int32), ("capacity", C.c_int32), ("reserved", C.c_int32)]
+
+
+_lib = None
+
+
+def load(path: Optional[str] = None):
+    """Load the HIP library (raises if it has not been built)."""
+    global _lib
+    if _lib is not None and path is None:
+        return _lib
+    p = path or LIB_PATH
+    if not os.path.exists(p):
+        raise RuntimeError(f"{p} is missing: build it with `python -m paper_2504_06419_amd.build`")
+    L = C.CDLL(p)
+    vp, i32, sz = C.c_void_p, C.c_int32, C.c_size_t
+    L.spire_verify_workspace_size.restype = sz
+    L.spire_verify_workspace_size.argtypes = [i32] * 5
+    L.spire_verify_attn.restype = C.c_int
+    L.spire_verify_attn.argtypes = [vp, i32, C.POINTER(KV), vp, i32, i32, i32, i32, i32, C.c_float,
+                                    vp, i32, vp, vp, sz, vp]
+    L.spire_draft_workspace_size.restype = sz
+    L.spire_draft_workspace_size.argtypes = [i32] * 4
+    L.spire_draft_sparse_attn.restype = C.c_int
+    L.spire_draft_sparse_attn.argtypes = [vp, i32, C.POINTER(KV), C.POINTER(KV), vp, vp, i32, i32,
+                                          i32, i32, i32, i32, C.c_float, vp, i32, vp, vp, sz, vp]
+    L.spire_status_string.restype = C.c_char_p
+    L.spire_status_string.argtypes = [C.c_int]
+    L.spire_last_error.restype = C.c_char_p
+    L.spire_last_error.argtypes = []
+    L.spire_version.restype = i32
+    L.spire_set_kernel_variant.restype = C.c_int
+    L.spire_set_kernel_variant.argtypes = [i32]
+    L.spire_timing_enable.restype = C.c_int
+    L.spire_timing_enable.argtypes = [i32]
+    L.spire_timing_collect.restype = i32
+    L.spire_timing_collect.argtypes = [vp, vp, i32]
+    if path is None:
+        _lib = L
+    return L
+
+
+def _check(rc: int):
+    if rc != 0:
+        raise SpireError(rc, load().spire_last_error().decode())
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else t.data_ptr()
+
+
+def _stream():
+    return torch.cuda.current_stream().cuda_stream
+
+
+def kv_view(k: torch.Tensor, v: torch.Tensor, block_table: Optional[torch.Tensor] = None,
+            page_size: int = 0, k_scale: Optional[torch.Tensor] = None,
+            v_scale: Optional[torch.Tensor] = None, capacity: Optional[int] = None) -> KV:
+    """Describe 4-d storage [blk, h, tok, d] (d contiguous) as a spire_kv.
+    Paged when `block_table` is given (blk = physical page), else contiguous
+    (blk = sequence, capacity = size of dim 2 unless given)."""
+    assert k.shape == v.shape and k.stride() == v.stride() and k.dtype == v.dtype
+    assert k.stride(3) == 1, "head dim must be contiguous"
+    kv = KV()
+    kv.k, kv.v = k.data_ptr(), v.data_ptr()
+    kv.s_blk, kv.s_head, kv.s_tok = k.stride(0), k.stride(1), k.stride(2)
+    kv.dtype = _DT[k.dtype]
+    kv.k_scale, kv.v_scale = _ptr(k_scale), _ptr(v_scale)
+    if block_table is not None:
+        assert block_table.dtype == torch.int32 and block_table.is_contiguous()
+        kv.block_table = block_table.data_ptr()
+        kv.page_size = page_size or k.shape[2]
+        kv.max_blocks = block_table.shape[1]
+        kv.num_blocks = k.shape[0]
+        kv.capacity = 0
+    else:
+        kv.block_table = None
+        kv.page_size = 0
+        kv.capacity = k.shape[2] if capacity is None else capacity
+    kv.reserved = 0
+    return kv
+
+
+def verify_workspace_size(B, Hq, Hkv, D, k) -> int:
+    return int(load().spire_verify_workspace_size(B, Hq, Hkv, D, k))
+
+
+def draft_workspace_size(B, Hq, Hkv, D) -> int:
+    return int(load().spire_draft_workspace_size(B, Hq, Hkv, D))
+
+
+def workspace(nbytes: int, device=None) -> torch.Tensor:
+    """A caller-owned workspace buffer (256-byte aligned by the caching allocator)."""
+    return torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device or "cuda")
+
+
+def verify_attn(q: torch.Tensor, kv: KV, kv_lens: torch.Tensor, Hkv: int, k: int,
+                sm_scale: float, out: Optional[torch.Tensor] = None,
+                lse: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,
+                out_dtype=torch.float32, with_lse: bool = True):
+    """spire_verify_attn.  q [B, k+1, Hq, D]; returns (out, lse)."""
+    B, nq, Hq, D = q.shape
+    assert nq == k + 1 and q.is_contiguous()
+    if out is None:
+        out = torch.empty((B, nq, Hq, D), dtype=out_dtype, device=q.device)
+    if lse is None and with_lse:
+        lse = torch.empty((B, nq, Hq), dtype=torch.float32, device=q.device)
+    if ws is None:
+        ws = workspace(verify_workspace_size(B, Hq, Hkv, D, k), q.device)
+    lens = kv_lens if kv_lens.dtype == torch.int32 else kv_lens.to(torch.int32)
+    _check(load().spire_verify_attn(q.data_ptr(), _DT[q.dtype], C.byref(kv), lens.data_ptr(), B, Hq,
+                                    Hkv, D, k, float(sm_scale), out.data_ptr(), _DT[out.dtype],
+                                    _ptr(lse), ws.data_ptr(), ws.numel(), _stream()))
+    return out, lse
+
+
+def draft_sparse_attn(q: torch.Tensor, sink: KV, ring: KV, seq_lens: torch.Tensor,
+                      ring_offset: torch.Tensor, S: int, W: int, sm_scale: float, Hkv: int,
+                      out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None,
+                      ws: Optional[torch.Tensor] = None, out_dtype=torch.float32,
+                      with_lse: bool = True):
+    """spire_draft_sparse_attn.  q [B, Hq, D]; returns (out, lse)."""
+    B, Hq, D = q.shape
+    assert q.is_contiguous()
+    if out is None:
+        out = torch.empty((B, Hq, D), dtype=out_dtype, device=q.device)
+    if lse is None and with_lse:
+        lse = torch.empty((B, Hq), dtype=torch.float32, device=q.device)
+    if ws is None:
+        ws = workspace(draft_workspace_size(B, Hq, Hkv, D), q.device)
+    _check(load().spire_draft_sparse_attn(q.data_ptr(), _DT[q.dtype], C.byref(sink), C.byref(ring),
+                                          seq_lens.data_ptr(), ring_offset.data_ptr(), B, Hq, Hkv,
+                                          D, S, W, float(sm_scale), out.data_ptr(), _DT[out.dtype],
+                                          _ptr(lse), ws.data_ptr(), ws.numel(), _stream()))
+    return out, lse
+
+
+def set_kernel_variant(variant: int):
+    _check(load().spire_set_kernel_variant(variant))
+
+
+def timing_enable(on: bool):
+    _check(load().spire_timing_enable(1 if on else 0))
+
+
+def timing_collect(max_records: int = 4096):
+    """[(kernel name, ms)] of the launches recorded since the last collect."""
+    ids = (C.c_int32 * max_records)()
+    ms = (C.c_float * max_records)()
+    n = load().spire_timing_collect(C.addressof(ids), C.addressof(ms), max_records)
+    return [(KERNEL_IDS.get(ids[i], str(ids[i])), float(ms[i])) for i in range(n)]

@@ -212,12 +212,12 @@ def make_verify_inputs(spec: VerifySpec, seed: int, device="cpu", keep_logical: 
         total = sum(blocks)
         phys = total + spec.spare_pages
         perm = torch.randperm(phys, generator=meta).tolist()
+        perm_t = torch.tensor(perm, dtype=torch.int32)
         table = torch.full((B, max_blocks), -1, dtype=torch.int32)
         pos = 0
         for b in range(B):
-            for j in range(blocks[b]):
-                table[b, j] = perm[pos]
-                pos += 1
+            table[b, : blocks[b]] = perm_t[pos: pos + blocks[b]]
+            pos += blocks[b]
         store_shape = (phys, Hkv, ps, D)
         capacity = max_blocks * ps
     else:
@@ -285,6 +285,16 @@ def _fill_poison(t: torch.Tensor, dtype: str, kind: Optional[str]):
         t.fill_(val)
 
 
+def _fill_poison_rows(t: torch.Tensor, rows: torch.Tensor, dtype: str, kind: Optional[str]):
+    """Poison rows `rows` of dim 1 of a [H, rows, D] tensor."""
+    if kind is None:
+        return
+    if dtype == "fp8":
+        t.view(torch.uint8)[:, rows] = 0x7F if kind == "nan" else 0x7E
+    else:
+        t[:, rows] = poison_value(dtype, kind)
+
+
 def _poison_unused_verify(kc, vc, n, table, ps, dtype, kind):
     """Write the poison value into every storage row no sequence exposes."""
     if ps > 0:
@@ -292,6 +302,8 @@ def _poison_unused_verify(kc, vc, n, table, ps, dtype, kind):
         tbl = table.cpu()
         for b, nb in enumerate(n):
             nblk = (nb + ps - 1) // ps
+            if nblk == 0:
+                continue
             ids = tbl[b, :nblk].long()
             used[ids] = True
             last = int(tbl[b, nblk - 1])
@@ -299,10 +311,14 @@ def _poison_unused_verify(kc, vc, n, table, ps, dtype, kind):
             if tail < ps:
                 _fill_poison(kc[last, :, tail:], dtype, kind)
                 _fill_poison(vc[last, :, tail:], dtype, kind)
-        spare = (~used).nonzero().flatten().tolist()
-        for p in spare:
-            _fill_poison(kc[p], dtype, kind)
-            _fill_poison(vc[p], dtype, kind)
+        spare = (~used).nonzero().flatten().to(kc.device)
+        if spare.numel():
+            if dtype == "fp8":
+                kc.view(torch.uint8)[spare] = 0x7F if kind == "nan" else 0x7E
+                vc.view(torch.uint8)[spare] = 0x7F if kind == "nan" else 0x7E
+            else:
+                kc[spare] = poison_value(dtype, kind)
+                vc[spare] = poison_value(dtype, kind)
     else:
         for b, nb in enumerate(n):
             if nb < kc.shape[2]:
@@ -397,10 +413,10 @@ def make_draft_inputs(spec: DraftSpec, seed: int, device="cpu", keep_logical: bo
                     _fill_poison(sink_v[b, :, L:], spec.kv_dtype, poison)
                 nvalid = max(0, L - S)
                 if nvalid < W:  # slots never written so far
-                    for j in range(nvalid, W):
-                        s = (int(offs[b]) + j) % W
-                        _fill_poison(ring_k[b, :, s], spec.kv_dtype, poison)
-                        _fill_poison(ring_v[b, :, s], spec.kv_dtype, poison)
+                    slots = (torch.arange(nvalid, W) + int(offs[b])) % W
+                    slots = slots.to(ring_k.device)
+                    _fill_poison_rows(ring_k[b], slots, spec.kv_dtype, poison)
+                    _fill_poison_rows(ring_v[b], slots, spec.kv_dtype, poison)
     return DraftInputs(spec=spec, q=q, sink_k=sink_k, sink_v=sink_v, ring_k=ring_k, ring_v=ring_v,
                        new_k=new_k, new_v=new_v, base_lens=base,
                        ring_offset=offs.to(torch.int32).to(device),

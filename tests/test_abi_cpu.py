@@ -1,0 +1,138 @@
+"""C ABI checks that need no GPU: the library loads, exports every function
+include/spire.h declares, and rejects invalid arguments on the host before
+enqueueing anything (no device pointer is dereferenced on these paths)."""
+import ctypes as C
+import os
+import re
+import subprocess
+
+import pytest
+
+from paper_2504_06419_amd import spire
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "spire.h")
+
+OK, INVALID, UNSUPPORTED, WORKSPACE, HIPERR = 0, 1, 2, 3, 4
+FAKE = 0x10000  # a 256-byte-aligned non-null address; never dereferenced here
+
+
+def header_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(spire_[a-z_]+)\s*\(", src)))
+
+
+def test_header_declares_the_binding_symbols():
+    assert header_functions() == sorted(spire.SYMBOLS)
+
+
+def test_library_exports_every_declared_symbol():
+    L = spire.load()
+    for name in header_functions():
+        assert hasattr(L, name), name
+    out = subprocess.run(["nm", "-D", "--defined-only", spire.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = set(re.findall(r"\sT\s(spire_\w+)", out))
+    assert set(header_functions()) <= exported
+
+
+def test_version_and_status_strings():
+    L = spire.load()
+    assert L.spire_version() == 1
+    for code, name in spire.STATUS.items():
+        assert L.spire_status_string(code).decode() == name
+    assert L.spire_status_string(99).decode() == "SPIRE_ERR_UNKNOWN"
+
+
+def kv(dtype=spire.BF16, page_size=0, capacity=64, table=None, scales=False, reserved=0):
+    d = spire.KV()
+    d.k, d.v = FAKE, FAKE
+    d.block_table = table
+    d.k_scale = FAKE if scales else None
+    d.v_scale = FAKE if scales else None
+    d.s_blk, d.s_head, d.s_tok = 8 * capacity * 128, capacity * 128, 128
+    d.dtype, d.page_size = dtype, page_size
+    d.max_blocks = 4 if table else 0
+    d.num_blocks = 16 if table else 0
+    d.capacity = capacity
+    d.reserved = reserved
+    return d
+
+
+def verify(**kw):
+    a = dict(q=FAKE, q_dtype=spire.BF16, kv=kv(), lens=FAKE, B=2, Hq=32, Hkv=8, D=128, k=4,
+             out=FAKE, out_dtype=spire.F32, lse=None, ws=FAKE, ws_bytes=1 << 30)
+    a.update(kw)
+    L = spire.load()
+    kvp = None if a["kv"] is None else C.byref(a["kv"])
+    return L.spire_verify_attn(a["q"], a["q_dtype"], kvp, a["lens"], a["B"], a["Hq"], a["Hkv"],
+                               a["D"], a["k"], 0.1, a["out"], a["out_dtype"], a["lse"], a["ws"],
+                               a["ws_bytes"], None)
+
+
+def draft(**kw):
+    a = dict(q=FAKE, q_dtype=spire.BF16, sink=kv(capacity=4), ring=kv(capacity=64), lens=FAKE,
+             offs=FAKE, B=2, Hq=32, Hkv=8, D=128, S=4, W=64, out=FAKE, ws=FAKE)
+    a.update(kw)
+    L = spire.load()
+    return L.spire_draft_sparse_attn(a["q"], a["q_dtype"], C.byref(a["sink"]), C.byref(a["ring"]),
+                                     a["lens"], a["offs"], a["B"], a["Hq"], a["Hkv"], a["D"],
+                                     a["S"], a["W"], 0.1, a["out"], spire.F32, None, a["ws"],
+                                     1 << 30, None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(B=-1), INVALID),
+    (dict(Hq=30), INVALID),
+    (dict(Hkv=0), INVALID),
+    (dict(D=96), UNSUPPORTED),
+    (dict(k=16), UNSUPPORTED),
+    (dict(k=-1), UNSUPPORTED),
+    (dict(Hq=128, Hkv=1, k=1), UNSUPPORTED),        # (k+1) * g = 256 rows
+    (dict(q_dtype=spire.FP8), UNSUPPORTED),
+    (dict(out_dtype=spire.FP8), UNSUPPORTED),
+    (dict(q=None), INVALID),
+    (dict(out=None), INVALID),
+    (dict(ws=None), WORKSPACE),
+    (dict(ws=FAKE + 16), WORKSPACE),                  # not 256-byte aligned
+    (dict(q=FAKE + 2), INVALID),                      # not 16-byte aligned
+    (dict(kv=None), INVALID),
+    (dict(kv=kv(dtype=7)), INVALID),
+    (dict(kv=kv(reserved=1)), INVALID),
+    (dict(kv=kv(dtype=spire.FP8)), INVALID),          # fp8 without scales
+    (dict(kv=kv(page_size=16)), INVALID),             # paged without a block table
+    (dict(kv=kv(capacity=0)), INVALID),
+    (dict(lens=None), INVALID),
+    (dict(B=9000), UNSUPPORTED),
+])
+def test_verify_rejects_invalid_arguments(kw, status):
+    assert verify(**kw) == status
+    assert spire.load().spire_last_error().decode() != ""
+
+
+def test_verify_empty_batch_is_a_no_op():
+    assert verify(B=0, q=None, out=None, ws=None, lens=None) == OK
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(S=0, W=0), INVALID),
+    (dict(S=-1), INVALID),
+    (dict(S=8), INVALID),                            # sink capacity 4 < S
+    (dict(W=128), INVALID),                          # ring capacity 64 < W
+    (dict(sink=kv(dtype=spire.F32, capacity=4)), INVALID),   # dtypes differ
+    (dict(ring=kv(page_size=16, table=FAKE)), UNSUPPORTED),  # paged ring
+    (dict(lens=None), INVALID),
+    (dict(offs=None), INVALID),
+    (dict(D=80), UNSUPPORTED),
+])
+def test_draft_rejects_invalid_arguments(kw, status):
+    assert draft(**kw) == status
+
+
+def test_kernel_variant_and_sizes():
+    L = spire.load()
+    assert L.spire_set_kernel_variant(2) == INVALID
+    assert L.spire_set_kernel_variant(0) == OK
+    assert L.spire_verify_workspace_size(4, 30, 8, 128, 4) == 0
+    assert L.spire_draft_workspace_size(4, 32, 0, 128) == 0
