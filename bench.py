@@ -89,31 +89,31 @@ def make_step(v, d):
     tokens = 0
     dominant = None
     if d is not None:
-        s = d.spec
+        ds = d.spec
         sink = spire.kv_view(d.sink_k, d.sink_v, k_scale=d.k_scale, v_scale=d.v_scale)
         ring = spire.kv_view(d.ring_k, d.ring_v, k_scale=d.k_scale, v_scale=d.v_scale)
-        ws = spire.workspace(spire.draft_workspace_size(s.B, s.Hq, s.Hkv, s.D))
-        out = torch.empty((s.B, s.Hq, s.D), dtype=torch.float32, device=d.q.device)
-        lse = torch.empty((s.B, s.Hq), dtype=torch.float32, device=d.q.device)
-        qs = [d.q[t].contiguous() for t in range(s.steps)]
-        lens = [d.seq_lens(t) for t in range(s.steps)]
-        for t in range(s.steps):
+        dws = spire.workspace(spire.draft_workspace_size(ds.B, ds.Hq, ds.Hkv, ds.D))
+        dout = torch.empty((ds.B, ds.Hq, ds.D), dtype=torch.float32, device=d.q.device)
+        dlse = torch.empty((ds.B, ds.Hq), dtype=torch.float32, device=d.q.device)
+        qs = [d.q[t].contiguous() for t in range(ds.steps)]
+        lens = [d.seq_lens(t) for t in range(ds.steps)]
+        for t in range(ds.steps):
             calls.append(lambda t=t: spire.draft_sparse_attn(qs[t], sink, ring, lens[t],
-                                                             d.ring_offset, s.S, s.W, d.sm_scale,
-                                                             s.Hkv, out=out, lse=lse, ws=ws))
+                                                             d.ring_offset, ds.S, ds.W, d.sm_scale,
+                                                             ds.Hkv, out=dout, lse=dlse, ws=dws))
             nbytes += draft_step_bytes(d, t)
-        tokens = s.B * s.steps
+        tokens = ds.B * ds.steps
         dominant = "draft_partial"
     if v is not None:
-        s = v.spec
+        vs = v.spec
         kv = spire.kv_view(v.k_cache, v.v_cache, v.block_table, v.page_size, v.k_scale, v.v_scale)
-        ws = spire.workspace(spire.verify_workspace_size(s.B, s.Hq, s.Hkv, s.D, s.k))
-        out = torch.empty((s.B, s.k + 1, s.Hq, s.D), dtype=torch.float32, device=v.q.device)
-        lse = torch.empty((s.B, s.k + 1, s.Hq), dtype=torch.float32, device=v.q.device)
-        calls.append(lambda: spire.verify_attn(v.q, kv, v.kv_lens, s.Hkv, s.k, v.sm_scale, out=out,
-                                               lse=lse, ws=ws))
+        vws = spire.workspace(spire.verify_workspace_size(vs.B, vs.Hq, vs.Hkv, vs.D, vs.k))
+        vout = torch.empty((vs.B, vs.k + 1, vs.Hq, vs.D), dtype=torch.float32, device=v.q.device)
+        vlse = torch.empty((vs.B, vs.k + 1, vs.Hq), dtype=torch.float32, device=v.q.device)
+        calls.append(lambda: spire.verify_attn(v.q, kv, v.kv_lens, vs.Hkv, vs.k, v.sm_scale,
+                                               out=vout, lse=vlse, ws=vws))
         nbytes += verify_bytes(v)
-        tokens = s.B * (s.k + 1)
+        tokens = vs.B * (vs.k + 1)
         if dominant is None or verify_bytes(v) > nbytes - verify_bytes(v):
             dominant = "verify_partial"
 

@@ -141,6 +141,8 @@ size_t spire_draft_workspace_size(int32_t B, int32_t Hq, int32_t Hkv, int32_t D)
  *   ring     contiguous view (page_size 0, capacity >= W) of W slots: logical
  *            position p >= S lives in slot (ring_offset[b] + p - S) mod W.
  *            sink and ring have the same dtype (fp8: each view's own scales).
+ *            The sink view may have NULL k/v when S == 0, the ring view when
+ *            W == 0 (they are never read then).
  *   seq_lens [B] int32: m_b, the number of logical positions including the
  *            query's own token (the caller has written it to the cache).
  *            Visible positions: [0, min(S, m_b)) U [max(S, m_b - W), m_b),

@@ -39,6 +39,8 @@ typedef __bf16 bf16x2 __attribute__((__vector_size__(4)));
 
 enum { MODE_CONTIG = 0, MODE_PAGED = 1, MODE_DRAFT = 2 };
 
+constexpr float kRescaleLog2 = 8.f;
+
 __device__ __forceinline__ f32x4 mfma_bf16(u32x4 a, u32x4 b, f32x4 c) {
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
                                                    __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
@@ -63,6 +65,15 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
     return __builtin_bit_cast(uint32_t, v);
 }
 
+// K/V rows are streamed once: nontemporal loads (the streaming cache policy)
+// keep them from displacing anything in L2 and measurably raise HBM read rate.
+__device__ __forceinline__ u32x4 ld16(const uint8_t *p) {
+    return __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(p));
+}
+__device__ __forceinline__ u32x2 ld8(const uint8_t *p) {
+    return __builtin_nontemporal_load(reinterpret_cast<const u32x2 *>(p));
+}
+
 template <bool FP8> struct TileRegs;
 template <> struct TileRegs<false> { u32x4 k[2][4]; u32x4 v[8]; };  // bf16
 template <> struct TileRegs<true> { u32x4 k[2][2]; u32x2 v[8]; };   // fp8
@@ -75,7 +86,7 @@ struct SegAddr {
     int64_t blk_bytes;               // paged: bytes per page (s_blk * elem)
     int64_t tok_bytes, sink_tok_bytes;
     int32_t n;                       // keys of the segment
-    int32_t cap16;                   // contiguous: last 16-aligned group start
+    int32_t cap;                     // contiguous: rows per sequence
     int32_t ps, num_blocks;
     int32_t ns, rs, W;               // draft: sinks, first ring slot, window
 };
@@ -84,11 +95,10 @@ struct SegAddr {
 template <int MODE>
 __device__ __forceinline__ int64_t group_row_offset(const SegAddr &a, int key0) {
     if (MODE == MODE_CONTIG) {
-        const int row = key0 < a.cap16 ? key0 : a.cap16;
-        return (int64_t)row * a.tok_bytes;
+        return (int64_t)key0 * a.tok_bytes;  // caller guarantees key0 + 16 <= capacity
     } else {
         const int kk = key0 < a.n ? key0 : a.n - 1;
-        int page = a.table[kk / a.ps];
+        int page = uload(a.table, kk / a.ps);
         page = page < 0 ? 0 : (page >= a.num_blocks ? a.num_blocks - 1 : page);
         const int row = (key0 < a.n ? key0 : kk) % a.ps & ~15;
         return (int64_t)page * a.blk_bytes + (int64_t)row * a.tok_bytes;
@@ -125,11 +135,11 @@ __device__ __forceinline__ void load_tile(TileRegs<FP8> &T, const SegAddr &a, in
             if (FP8) {
 #pragma unroll
                 for (int u = 0; u < 2; ++u)
-                    T.k[mb][u] = *reinterpret_cast<const u32x4 *>(kp + 64 * u + 16 * j);
+                    T.k[mb][u] = ld16(kp + 64 * u + 16 * j);
             } else {
 #pragma unroll
                 for (int c = 0; c < 4; ++c)
-                    T.k[mb][c] = *reinterpret_cast<const u32x4 *>(kp + 64 * c + 16 * j);
+                    T.k[mb][c] = ld16(kp + 64 * c + 16 * j);
             }
         }
 #pragma unroll
@@ -137,9 +147,33 @@ __device__ __forceinline__ void load_tile(TileRegs<FP8> &T, const SegAddr &a, in
             const uint8_t *kp, *vp;
             draft_rows(a, key0 + 4 * t + j, kp, vp);
             if (FP8)
-                *reinterpret_cast<u32x2 *>(&T.v[t]) = *reinterpret_cast<const u32x2 *>(vp + 8 * n16);
+                *reinterpret_cast<u32x2 *>(&T.v[t]) = ld8(vp + 8 * n16);
             else
-                *reinterpret_cast<u32x4 *>(&T.v[t]) = *reinterpret_cast<const u32x4 *>(vp + 16 * n16);
+                *reinterpret_cast<u32x4 *>(&T.v[t]) = ld16(vp + 16 * n16);
+        }
+    } else if (MODE == MODE_CONTIG && key0 + kMfmaTile > a.cap) {
+        // last tile of a contiguous sequence whose capacity ends inside it:
+        // rows past the capacity are clamped per lane (their keys are masked)
+#pragma unroll
+        for (int mb = 0; mb < 2; ++mb) {
+            const int row = min(key0 + 16 * mb + rho, a.cap - 1);
+            const uint8_t *kp = a.kseq + (int64_t)row * a.tok_bytes + 16 * j;
+            if (FP8) {
+#pragma unroll
+                for (int u = 0; u < 2; ++u) T.k[mb][u] = ld16(kp + 64 * u);
+            } else {
+#pragma unroll
+                for (int c = 0; c < 4; ++c) T.k[mb][c] = ld16(kp + 64 * c);
+            }
+        }
+#pragma unroll
+        for (int t = 0; t < 8; ++t) {
+            const int row = min(key0 + 4 * t + j, a.cap - 1);
+            const uint8_t *vp = a.vseq + (int64_t)row * a.tok_bytes + (FP8 ? 8 : 16) * n16;
+            if (FP8)
+                *reinterpret_cast<u32x2 *>(&T.v[t]) = ld8(vp);
+            else
+                *reinterpret_cast<u32x4 *>(&T.v[t]) = ld16(vp);
         }
     } else {
         const int64_t g0 = group_row_offset<MODE>(a, key0);
@@ -150,10 +184,10 @@ __device__ __forceinline__ void load_tile(TileRegs<FP8> &T, const SegAddr &a, in
             const uint8_t *kp = a.kseq + (mb ? g1 : g0) + koff;
             if (FP8) {
 #pragma unroll
-                for (int u = 0; u < 2; ++u) T.k[mb][u] = *reinterpret_cast<const u32x4 *>(kp + 64 * u);
+                for (int u = 0; u < 2; ++u) T.k[mb][u] = ld16(kp + 64 * u);
             } else {
 #pragma unroll
-                for (int c = 0; c < 4; ++c) T.k[mb][c] = *reinterpret_cast<const u32x4 *>(kp + 64 * c);
+                for (int c = 0; c < 4; ++c) T.k[mb][c] = ld16(kp + 64 * c);
             }
         }
         const int64_t voff = (int64_t)j * a.tok_bytes + (FP8 ? 8 : 16) * n16;
@@ -161,9 +195,9 @@ __device__ __forceinline__ void load_tile(TileRegs<FP8> &T, const SegAddr &a, in
         for (int t = 0; t < 8; ++t) {
             const uint8_t *vp = a.vseq + (t < 4 ? g0 : g1) + (int64_t)(4 * (t & 3)) * a.tok_bytes + voff;
             if (FP8)
-                *reinterpret_cast<u32x2 *>(&T.v[t]) = *reinterpret_cast<const u32x2 *>(vp);
+                *reinterpret_cast<u32x2 *>(&T.v[t]) = ld8(vp);
             else
-                *reinterpret_cast<u32x4 *>(&T.v[t]) = *reinterpret_cast<const u32x4 *>(vp);
+                *reinterpret_cast<u32x4 *>(&T.v[t]) = ld16(vp);
         }
     }
 }
@@ -203,8 +237,12 @@ __device__ __forceinline__ void compute_tile(TileRegs<FP8> &T, const u32x4 (&qf)
     }
 
     // ---- mask, online softmax (base 2) ---------------------------------------
+    // The reference maximum of a row only moves when a tile exceeds it by more
+    // than kRescaleLog2 (probabilities stay <= 2^kRescaleLog2), so the
+    // accumulator rescale is skipped for almost every tile.
     const bool need_mask = key0 + kMfmaTile > full_lim;
     u32x4 pb[NB];
+    float alpha[NB];
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
         float x[2][4];
@@ -220,9 +258,10 @@ __device__ __forceinline__ void compute_tile(TileRegs<FP8> &T, const u32x4 (&qf)
             }
         mx = fmaxf(mx, __shfl_xor(mx, 16));
         mx = fmaxf(mx, __shfl_xor(mx, 32));
-        const float mnew = fmaxf(st.m[nb], mx);
+        const float mold = st.m[nb];
+        const float mnew = mx > mold + kRescaleLog2 ? mx : mold;
         const float msub = mnew == -INFINITY ? 0.f : mnew;
-        const float alpha = exp2f(st.m[nb] - msub);  // m = -inf -> 0
+        alpha[nb] = exp2f(mold - msub);  // 1 when unchanged, 0 from -inf
         st.m[nb] = mnew;
         float psum = 0.f;
 #pragma unroll
@@ -232,13 +271,21 @@ __device__ __forceinline__ void compute_tile(TileRegs<FP8> &T, const u32x4 (&qf)
                 x[mb][i] = exp2f(x[mb][i] - msub);
                 psum += x[mb][i];
             }
-        st.l[nb] = st.l[nb] * alpha + psum;
-#pragma unroll
-        for (int mb = 0; mb < 8; ++mb) st.acc[mb][nb] *= alpha;
+        st.l[nb] = st.l[nb] * alpha[nb] + psum;
         pb[nb].x = pack_bf16x2(x[0][0], x[0][1]);
         pb[nb].y = pack_bf16x2(x[0][2], x[0][3]);
         pb[nb].z = pack_bf16x2(x[1][0], x[1][1]);
         pb[nb].w = pack_bf16x2(x[1][2], x[1][3]);
+    }
+
+    bool rescale = false;
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) rescale |= alpha[nb] != 1.f;
+    if (__any(rescale)) {
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+            for (int mb = 0; mb < 8; ++mb) st.acc[mb][nb] *= alpha[nb];
     }
 
     // ---- V: keys beyond the segment end are zeroed (storage there may be anything)
@@ -281,21 +328,21 @@ __global__ __launch_bounds__(256, 1) void mfma_partial_kernel(Problem p, Plan pl
     const int n16 = lane & 15, j = lane >> 4;
     const int wid = __builtin_amdgcn_readfirstlane(blockIdx.x * kMfmaWavesPerWG + (threadIdx.x >> 6));
     if (wid >= pl.workers) return;
-    const int64_t T = (int64_t)pl.prefix[p.B] * pl.units;
+    const int64_t T = (int64_t)uload(pl.prefix, p.B) * pl.units;
     int64_t pos = worker_begin(wid, T, pl.workers);
     const int64_t end = worker_begin(wid + 1, T, pl.workers);
     if (pos >= end) return;
-    int seg = pl.wstart[2 * wid];
-    int tile = pl.wstart[2 * wid + 1];
+    int seg = uload(pl.wstart, 2 * wid);
+    int tile = uload(pl.wstart, 2 * wid + 1);
     const int64_t begin = pos;
 
     while (pos < end) {
         const int b = seg / pl.units;
         const int h = seg - b * pl.units;
-        const int tiles_b = pl.prefix[b + 1] - pl.prefix[b];
+        const int tiles_b = uload(pl.prefix, b + 1) - uload(pl.prefix, b);
         const int64_t left = end - pos;
         const int t1 = left < (int64_t)(tiles_b - tile) ? tile + (int)left : tiles_b;
-        const int n = pl.nkeys[b];
+        const int n = uload(pl.nkeys, b);
 
         // ---- segment addressing ------------------------------------------------
         SegAddr a;
@@ -312,21 +359,22 @@ __global__ __launch_bounds__(256, 1) void mfma_partial_kernel(Problem p, Plan pl
             const int64_t off = ((int64_t)b * p.kv.s_blk + (int64_t)h * p.kv.s_head) * p.kv.elem;
             a.kseq = p.kv.k + off;
             a.vseq = p.kv.v + off;
-            a.cap16 = p.kv.capacity - 16;
+            a.cap = p.kv.capacity;
         }
         if (MODE == MODE_DRAFT) {
             const int64_t soff = ((int64_t)b * p.sink.s_blk + (int64_t)h * p.sink.s_head) * p.sink.elem;
             a.ksink = p.sink.k + soff;
             a.vsink = p.sink.v + soff;
             a.sink_tok_bytes = p.sink.s_tok * p.sink.elem;
-            const int m = p.lens[b] < 0 ? 0 : p.lens[b];
+            const int mraw = uload(p.lens, b);
+            const int m = mraw < 0 ? 0 : mraw;
             a.ns = m < p.S ? m : p.S;
             a.W = p.W;
             int first = m - p.S - p.W;  // first valid logical ring index
             first = first < 0 ? 0 : first;
             int o = 0;
             if (p.W > 0) {
-                o = p.ring_offset[b] % p.W;
+                o = uload(p.ring_offset, b) % p.W;
                 if (o < 0) o += p.W;
                 o = (n - a.ns == p.W) ? 0 : (o + first % p.W) % p.W;  // full ring: physical order
             }
@@ -355,7 +403,7 @@ __global__ __launch_bounds__(256, 1) void mfma_partial_kernel(Problem p, Plan pl
             }
         }
         float sc = p.sm_scale_log2;
-        if (FP8) sc *= p.kv.k_scale[h];
+        if (FP8) sc *= uload(p.kv.k_scale, h);
 
         // ---- tiles [tile, t1): three register buffers, two tiles in flight ----
         if (n > 0) {
@@ -380,7 +428,7 @@ __global__ __launch_bounds__(256, 1) void mfma_partial_kernel(Problem p, Plan pl
         // ---- finalize: reduce the row sums over the 4 lane groups --------------
         const bool whole = (tile == 0 && t1 == tiles_b);
         const int64_t slot = 2 * (int64_t)wid + (pos == begin ? 0 : 1);
-        const float vs = FP8 ? p.kv.v_scale[h] : 1.f;
+        const float vs = FP8 ? uload(p.kv.v_scale, h) : 1.f;
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb) {
             float l = st.l[nb];

@@ -119,8 +119,10 @@ __global__ __launch_bounds__(256) void combine_kernel(Problem p, Plan pl) {
 
     for (int idx = threadIdx.x; idx < nrows * d4n; idx += blockDim.x) {
         const int r = idx / d4n, d4 = idx - (idx / d4n) * d4n;
+        // workers with an empty range (more workers than tiles) wrote nothing
         float M = -INFINITY;
         for (int64_t w = wlo; w <= whi; ++w) {
+            if (worker_begin(w + 1, T, pl.workers) == worker_begin(w, T, pl.workers)) continue;
             const int64_t slot = 2 * w + ((w == wlo && begin_lo < start) ? 1 : 0);
             M = fmaxf(M, pl.part_lse[slot * pl.rows + r]);
         }
@@ -128,6 +130,7 @@ __global__ __launch_bounds__(256) void combine_kernel(Problem p, Plan pl) {
         float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
         if (M != -INFINITY) {
             for (int64_t w = wlo; w <= whi; ++w) {
+                if (worker_begin(w + 1, T, pl.workers) == worker_begin(w, T, pl.workers)) continue;
                 const int64_t slot = 2 * w + ((w == wlo && begin_lo < start) ? 1 : 0);
                 const float lp = pl.part_lse[slot * pl.rows + r];
                 const float wgt = lp == -INFINITY ? 0.f : exp2f(lp - M);

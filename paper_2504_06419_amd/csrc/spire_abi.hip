@@ -113,15 +113,17 @@ int elem_size(int dt) {
     }
 }
 
-spire_status check_kv(const spire_kv *kv, const char *name, int D, int Hkv, bool allow_paged) {
+spire_status check_kv(const spire_kv *kv, const char *name, int D, int Hkv, bool allow_paged,
+                      bool read = true) {
     if (kv == nullptr) return fail(SPIRE_ERR_INVALID_ARG, "%s: descriptor is NULL", name);
-    if (kv->k == nullptr || kv->v == nullptr) return fail(SPIRE_ERR_INVALID_ARG, "%s: k or v is NULL", name);
+    if (read && (kv->k == nullptr || kv->v == nullptr))
+        return fail(SPIRE_ERR_INVALID_ARG, "%s: k or v is NULL", name);
     const int es = elem_size(kv->dtype);
     if (es == 0) return fail(SPIRE_ERR_INVALID_ARG, "%s: unknown dtype %d", name, kv->dtype);
     if (kv->reserved != 0) return fail(SPIRE_ERR_INVALID_ARG, "%s: reserved field must be 0", name);
     if (kv->s_blk < 0 || kv->s_head < 0 || kv->s_tok < 0)
         return fail(SPIRE_ERR_INVALID_ARG, "%s: negative stride", name);
-    if (kv->dtype == SPIRE_FP8_E4M3FN && (kv->k_scale == nullptr || kv->v_scale == nullptr))
+    if (read && kv->dtype == SPIRE_FP8_E4M3FN && (kv->k_scale == nullptr || kv->v_scale == nullptr))
         return fail(SPIRE_ERR_INVALID_ARG, "%s: fp8 storage needs k_scale and v_scale", name);
     if (kv->page_size < 0) return fail(SPIRE_ERR_INVALID_ARG, "%s: negative page_size", name);
     if (kv->page_size > 0) {
@@ -285,8 +287,7 @@ spire_status spire_verify_attn(const void *q, int32_t q_dtype, const spire_kv *k
     p.out_dtype = out_dtype;
     p.lse = lse;
 
-    const bool layout_ok = kv->page_size > 0 ? (kv->page_size % 16 == 0)
-                                             : (kv->capacity >= 16 && kv->capacity % 16 == 0);
+    const bool layout_ok = kv->page_size > 0 ? (kv->page_size % 16 == 0) : (kv->capacity >= 1);
     const bool mfma = (kv->dtype == SPIRE_BF16 || kv->dtype == SPIRE_FP8_E4M3FN) &&
                       q_dtype == SPIRE_BF16 && D == 128 && p.R <= 80 && layout_ok && rows_aligned(kv);
     return run(p, mfma, workspace, workspace_bytes, stream, 1);
@@ -303,9 +304,9 @@ spire_status spire_draft_sparse_attn(const void *q, int32_t q_dtype, const spire
     if (s != SPIRE_OK) return s;
     if (S < 0 || W < 0 || (int64_t)S + W < 1)
         return fail(SPIRE_ERR_INVALID_ARG, "need S >= 0, W >= 0, S + W >= 1 (S=%d, W=%d)", S, W);
-    s = check_kv(sink, "sink", D, Hkv, false);
+    s = check_kv(sink, "sink", D, Hkv, false, S > 0);
     if (s != SPIRE_OK) return s;
-    s = check_kv(ring, "ring", D, Hkv, false);
+    s = check_kv(ring, "ring", D, Hkv, false, W > 0);
     if (s != SPIRE_OK) return s;
     if (sink->dtype != ring->dtype) return fail(SPIRE_ERR_INVALID_ARG, "sink and ring dtypes differ");
     if (sink->capacity < S) return fail(SPIRE_ERR_INVALID_ARG, "sink capacity %d < S = %d", sink->capacity, S);

@@ -75,6 +75,16 @@ struct Plan {
     int32_t workers;
 };
 
+// Read-only, wave-uniform metadata (block tables, prefix sums, lengths,
+// scales) is read through the constant address space so that it becomes a
+// scalar load: those are counted separately from the vector loads of K/V, so
+// waiting for a page id never forces waiting for K/V loads already in flight.
+template <class T>
+__device__ __forceinline__ T uload(const T *p, int64_t i) {
+    typedef const T __attribute__((address_space(4))) cT;
+    return ((const cT *)p)[i];
+}
+
 __device__ __forceinline__ int64_t worker_begin(int64_t w, int64_t T, int64_t workers) {
     return (w * T) / workers;
 }
