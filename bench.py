@@ -211,6 +211,46 @@ def run_cpu_baseline(v, d, budget_s: float):
 
 
 # ---------------------------------------------------------------------------
+KERNEL_SOURCES = ["paper_2504_06419_amd/csrc/attn_mfma.hip",
+                  "paper_2504_06419_amd/csrc/spire_internal.h"]
+
+
+def kernel_source_hash() -> str:
+    """sha256 over the sources of the attention kernels; recorded HBM traffic is
+    reported only while the kernels are the ones the counters were taken on."""
+    import hashlib
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        h.update(open(os.path.join(ROOT, f), "rb").read())
+    return h.hexdigest()
+
+
+def calibrate_copy(nbytes: int = 4 << 30, reps: int = 3):
+    """A plain device-to-device copy of known size (reads and writes `nbytes`):
+    the reference dispatch for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE."""
+    src = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    src.fill_(1)
+    torch.cuda.synchronize()
+    for _ in range(reps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"calibration_copy_bytes": nbytes, "reps": reps}), flush=True)
+
+
+def recorded_traffic(path: str, workload: str, kernel: str):
+    """HBM bytes per launch from the counter record, or None if absent/stale."""
+    if not os.path.exists(path):
+        return None
+    try:
+        ent = json.load(open(path)).get(workload, {})
+    except (ValueError, OSError):
+        return None
+    if ent.get("kernel") != kernel or ent.get("source_sha256") != kernel_source_hash():
+        return None
+    return ent.get("bytes_per_launch")
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -219,8 +259,14 @@ def main():
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD, choices=list(W.named_workloads()))
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--traffic-json", default=os.path.join(ROOT, "profiles", "traffic.json"))
+    ap.add_argument("--traffic-json", default=os.path.join(ROOT, "profiles", "hbm_traffic.json"))
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="only run a 4 GiB device copy (counter calibration) and exit")
+    ap.add_argument("--source-hash", action="store_true", help="print the kernel source hash")
     a = ap.parse_args()
+    if a.source_hash:
+        print(kernel_source_hash())
+        return
     if a.gpus != 1:
         print(f"bench.py measures one GPU only (asked for --gpus {a.gpus}); the multi-GPU sharding "
               "of this path is described in DESIGN.md and is not run.", file=sys.stderr)
@@ -230,6 +276,9 @@ def main():
         sys.exit(1)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if a.calibrate_copy:
+        calibrate_copy()
+        return
     spire.load()
     print(f"[bench] building workload {a.workload}", file=sys.stderr, flush=True)
     wl, v, d = build_workload(a.workload, dev)
@@ -269,15 +318,7 @@ def main():
     dom_bytes = dominant_bytes(v, d, dominant)
     achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
 
-    traffic = None
-    if os.path.exists(a.traffic_json):
-        try:
-            tj = json.load(open(a.traffic_json))
-            ent = tj.get(a.workload, {})
-            if ent.get("kernel") == dominant and ent.get("bytes_per_launch"):
-                traffic = ent["bytes_per_launch"]
-        except Exception:
-            traffic = None
+    traffic = recorded_traffic(a.traffic_json, a.workload, dominant)
 
     gbs = nbytes / (ms * 1e-3) / 1e9
     spec = (v or d).spec
