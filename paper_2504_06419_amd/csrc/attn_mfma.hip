@@ -18,15 +18,19 @@
 //   * The PV reduction index 8j+t is key 4t + j: exactly the S^T values lane l
 //     already holds (t < 4 from mb = 0, t >= 4 from mb = 1), so P never
 //     leaves its lane, and each V load instruction (t fixed) covers 4 whole,
-//     consecutive 256-byte key rows.
-//   * PV row m of dim block mb' is head dim 8m + mb', so lane l loads the 16
-//     contiguous bytes d = 8 n16 .. 8 n16 + 7 of each of its keys, transposes
+//     consecutive key rows.
+//   * PV row m of dim block mb' is head dim 8m + mb', so lane l loads the 8
+//     contiguous dims d = 8 n16 .. 8 n16 + 7 of each of its keys, transposes
 //     8 keys x 8 dims in registers (byte permutes), and ends up owning the 32
 //     contiguous output dims 32j .. 32j + 31 of its row.
-//   * K: lane l loads 64 contiguous bytes per key group row (16 B per call).
+//   * K: each load instruction covers 64 contiguous bytes of 16 key rows.
 // fp8 (OCP e4m3fn) K/V are converted to bf16 in registers (exact); the
 // per-head K scale is folded into the softmax scale, the V scale into the
-// final normalisation.  Three tiles are kept in registers (two in flight).
+// final normalisation.
+//
+// Up to 32 rows (NB <= 2) the queries stay in registers and three tiles are
+// kept in registers (two in flight); with more rows the queries are staged in
+// LDS and two tiles are kept, so nothing spills to scratch.
 #include "spire_internal.h"
 
 namespace spire {
@@ -78,47 +82,68 @@ template <bool FP8> struct TileRegs;
 template <> struct TileRegs<false> { u32x4 k[2][4]; u32x4 v[8]; };  // bf16
 template <> struct TileRegs<true> { u32x4 k[2][2]; u32x2 v[8]; };   // fp8
 
-// Per-segment addressing state (uniform values except the per-lane offsets).
+// Per-segment addressing state (uniform values).
 struct SegAddr {
-    const uint8_t *kseq, *vseq;      // contiguous: (b, h) base; paged: h offset applied
+    const uint8_t *kseq, *vseq;      // contiguous/ring: (b, h) base; paged: head offset applied
     const uint8_t *ksink, *vsink;    // draft sinks (b, h) base
     const int32_t *table;            // paged: block table row of b
-    int64_t blk_bytes;               // paged: bytes per page (s_blk * elem)
+    int64_t blk_bytes;               // paged: bytes per page
     int64_t tok_bytes, sink_tok_bytes;
     int32_t n;                       // keys of the segment
     int32_t cap;                     // contiguous: rows per sequence
-    int32_t ps, num_blocks;
-    int32_t ns, rs, W;               // draft: sinks, first ring slot, window
+    int32_t ps, num_blocks;          // paged
+    int32_t nr, rs, W;               // draft: valid ring slots, first slot, window
 };
 
-// base pointer of the 16-key group starting at key `key0` (uniform)
-template <int MODE>
-__device__ __forceinline__ int64_t group_row_offset(const SegAddr &a, int key0) {
-    if (MODE == MODE_CONTIG) {
-        return (int64_t)key0 * a.tok_bytes;  // caller guarantees key0 + 16 <= capacity
+template <bool FP8>
+__device__ __forceinline__ void load_k_row(TileRegs<FP8> &T, int mb, const uint8_t *kp) {
+    if (FP8) {
+#pragma unroll
+        for (int u = 0; u < 2; ++u) T.k[mb][u] = ld16(kp + 64 * u);
     } else {
+#pragma unroll
+        for (int c = 0; c < 4; ++c) T.k[mb][c] = ld16(kp + 64 * c);
+    }
+}
+template <bool FP8>
+__device__ __forceinline__ void load_v_row(TileRegs<FP8> &T, int t, const uint8_t *vp) {
+    if (FP8)
+        *reinterpret_cast<u32x2 *>(&T.v[t]) = ld8(vp);
+    else
+        *reinterpret_cast<u32x4 *>(&T.v[t]) = ld16(vp);
+}
+
+// Draft key space: keys [0, nr) are the valid ring slots starting at slot rs
+// (wrapping), keys [nr, nr + ns) the sink rows; keys beyond the segment are
+// clamped to a valid row (their scores are masked and values zeroed).
+// Branch-free (selects only), so that loads never sit under divergent control flow.
+__device__ __forceinline__ const uint8_t *draft_row(const SegAddr &a, int j, bool value) {
+    j = j < a.n ? j : (a.nr > 0 ? 0 : a.n - 1);
+    const bool sink = j >= a.nr;
+    int s = a.rs + j;
+    s = s >= a.W ? s - a.W : s;
+    const uint8_t *ring = (value ? a.vseq : a.kseq) + (int64_t)s * a.tok_bytes;
+    const uint8_t *snk = (value ? a.vsink : a.ksink) + (int64_t)(j - a.nr) * a.sink_tok_bytes;
+    return sink ? snk : ring;
+}
+
+// Base byte offset of the contiguous 16-key group starting at key0, or -1 if
+// the group is not one contiguous run of rows (only then per-lane addressing).
+template <int MODE>
+__device__ __forceinline__ int64_t group_base(const SegAddr &a, int key0) {
+    if (MODE == MODE_CONTIG) {
+        return key0 + 16 <= a.cap ? (int64_t)key0 * a.tok_bytes : -1;
+    } else if (MODE == MODE_PAGED) {
         const int kk = key0 < a.n ? key0 : a.n - 1;
         int page = uload(a.table, kk / a.ps);
         page = page < 0 ? 0 : (page >= a.num_blocks ? a.num_blocks - 1 : page);
-        const int row = (key0 < a.n ? key0 : kk) % a.ps & ~15;
+        const int row = (kk % a.ps) & ~15;
         return (int64_t)page * a.blk_bytes + (int64_t)row * a.tok_bytes;
-    }
-}
-
-// draft: storage row of key j (per lane)
-__device__ __forceinline__ void draft_rows(const SegAddr &a, int j, const uint8_t *&kp,
-                                           const uint8_t *&vp) {
-    if (j < a.ns) {
-        kp = a.ksink + (int64_t)j * a.sink_tok_bytes;
-        vp = a.vsink + (int64_t)j * a.sink_tok_bytes;
-    } else if (a.W > 0) {
-        int s = a.rs + (j - a.ns);
-        while (s >= a.W) s -= a.W;
-        kp = a.kseq + (int64_t)s * a.tok_bytes;
-        vp = a.vseq + (int64_t)s * a.tok_bytes;
     } else {
-        kp = a.ksink + (int64_t)(a.ns - 1) * a.sink_tok_bytes;
-        vp = a.vsink + (int64_t)(a.ns - 1) * a.sink_tok_bytes;
+        if (key0 + 16 > a.nr) return -1;
+        int s = a.rs + key0;
+        if (s >= a.W) s -= a.W;
+        return s + 16 <= a.W ? (int64_t)s * a.tok_bytes : -1;
     }
 }
 
@@ -127,78 +152,40 @@ __device__ __forceinline__ void load_tile(TileRegs<FP8> &T, const SegAddr &a, in
     const int n16 = lane & 15, j = lane >> 4;
     const int rho = 4 * (n16 & 3) + (n16 >> 2);
     const int key0 = tile * kMfmaTile;
-    if (MODE == MODE_DRAFT) {
+    const int64_t g0 = group_base<MODE>(a, key0);
+    const int64_t g1 = group_base<MODE>(a, key0 + 16);
+    const int64_t koff = (int64_t)rho * a.tok_bytes + 16 * j;
+    const int64_t voff = (int64_t)j * a.tok_bytes + (FP8 ? 8 : 16) * n16;
+    if (MODE == MODE_PAGED || (g0 >= 0 && g1 >= 0)) {  // fast path: two contiguous 16-row groups
 #pragma unroll
-        for (int mb = 0; mb < 2; ++mb) {
-            const uint8_t *kp, *vp;
-            draft_rows(a, key0 + 16 * mb + rho, kp, vp);
-            if (FP8) {
+        for (int mb = 0; mb < 2; ++mb) load_k_row<FP8>(T, mb, a.kseq + (mb ? g1 : g0) + koff);
 #pragma unroll
-                for (int u = 0; u < 2; ++u)
-                    T.k[mb][u] = ld16(kp + 64 * u + 16 * j);
-            } else {
+        for (int t = 0; t < 8; ++t)
+            load_v_row<FP8>(T, t, a.vseq + (t < 4 ? g0 : g1) + (int64_t)(4 * (t & 3)) * a.tok_bytes + voff);
+        return;
+    }
+    // per-lane rows: contiguous tails past the capacity, ring wrap, sinks
 #pragma unroll
-                for (int c = 0; c < 4; ++c)
-                    T.k[mb][c] = ld16(kp + 64 * c + 16 * j);
-            }
+    for (int mb = 0; mb < 2; ++mb) {
+        const int key = key0 + 16 * mb + rho;
+        const uint8_t *kp;
+        if (MODE == MODE_DRAFT) {
+            kp = draft_row(a, key, false) + 16 * j;
+        } else {
+            kp = a.kseq + (int64_t)min(key, a.cap - 1) * a.tok_bytes + 16 * j;
         }
+        load_k_row<FP8>(T, mb, kp);
+    }
 #pragma unroll
-        for (int t = 0; t < 8; ++t) {
-            const uint8_t *kp, *vp;
-            draft_rows(a, key0 + 4 * t + j, kp, vp);
-            if (FP8)
-                *reinterpret_cast<u32x2 *>(&T.v[t]) = ld8(vp + 8 * n16);
-            else
-                *reinterpret_cast<u32x4 *>(&T.v[t]) = ld16(vp + 16 * n16);
+    for (int t = 0; t < 8; ++t) {
+        const int key = key0 + 4 * t + j;
+        const uint8_t *vp;
+        if (MODE == MODE_DRAFT) {
+            vp = draft_row(a, key, true) + (FP8 ? 8 : 16) * n16;
+        } else {
+            vp = a.vseq + (int64_t)min(key, a.cap - 1) * a.tok_bytes + (FP8 ? 8 : 16) * n16;
         }
-    } else if (MODE == MODE_CONTIG && key0 + kMfmaTile > a.cap) {
-        // last tile of a contiguous sequence whose capacity ends inside it:
-        // rows past the capacity are clamped per lane (their keys are masked)
-#pragma unroll
-        for (int mb = 0; mb < 2; ++mb) {
-            const int row = min(key0 + 16 * mb + rho, a.cap - 1);
-            const uint8_t *kp = a.kseq + (int64_t)row * a.tok_bytes + 16 * j;
-            if (FP8) {
-#pragma unroll
-                for (int u = 0; u < 2; ++u) T.k[mb][u] = ld16(kp + 64 * u);
-            } else {
-#pragma unroll
-                for (int c = 0; c < 4; ++c) T.k[mb][c] = ld16(kp + 64 * c);
-            }
-        }
-#pragma unroll
-        for (int t = 0; t < 8; ++t) {
-            const int row = min(key0 + 4 * t + j, a.cap - 1);
-            const uint8_t *vp = a.vseq + (int64_t)row * a.tok_bytes + (FP8 ? 8 : 16) * n16;
-            if (FP8)
-                *reinterpret_cast<u32x2 *>(&T.v[t]) = ld8(vp);
-            else
-                *reinterpret_cast<u32x4 *>(&T.v[t]) = ld16(vp);
-        }
-    } else {
-        const int64_t g0 = group_row_offset<MODE>(a, key0);
-        const int64_t g1 = group_row_offset<MODE>(a, key0 + 16);
-        const int64_t koff = (int64_t)rho * a.tok_bytes + 16 * j;
-#pragma unroll
-        for (int mb = 0; mb < 2; ++mb) {
-            const uint8_t *kp = a.kseq + (mb ? g1 : g0) + koff;
-            if (FP8) {
-#pragma unroll
-                for (int u = 0; u < 2; ++u) T.k[mb][u] = ld16(kp + 64 * u);
-            } else {
-#pragma unroll
-                for (int c = 0; c < 4; ++c) T.k[mb][c] = ld16(kp + 64 * c);
-            }
-        }
-        const int64_t voff = (int64_t)j * a.tok_bytes + (FP8 ? 8 : 16) * n16;
-#pragma unroll
-        for (int t = 0; t < 8; ++t) {
-            const uint8_t *vp = a.vseq + (t < 4 ? g0 : g1) + (int64_t)(4 * (t & 3)) * a.tok_bytes + voff;
-            if (FP8)
-                *reinterpret_cast<u32x2 *>(&T.v[t]) = ld8(vp);
-            else
-                *reinterpret_cast<u32x4 *>(&T.v[t]) = ld16(vp);
-        }
+        load_v_row<FP8>(T, t, vp);
     }
 }
 
@@ -209,8 +196,21 @@ template <int NB> struct SoftmaxState {
     int lim[NB];
 };
 
-template <bool FP8, int NB>
-__device__ __forceinline__ void compute_tile(TileRegs<FP8> &T, const u32x4 (&qf)[NB][4],
+// Query fragments: registers for NB <= 2, LDS (lane-private slots) beyond.
+template <int NB, bool QLDS> struct QFrag;
+template <int NB> struct QFrag<NB, false> {
+    u32x4 r[NB][4];
+    __device__ __forceinline__ void put(int nb, int c, u32x4 v, int) { r[nb][c] = v; }
+    __device__ __forceinline__ u32x4 get(int nb, int c, int) const { return r[nb][c]; }
+};
+template <int NB> struct QFrag<NB, true> {
+    u32x4 *lds;  // [NB][4][64] of this wave
+    __device__ __forceinline__ void put(int nb, int c, u32x4 v, int lane) { lds[(nb * 4 + c) * 64 + lane] = v; }
+    __device__ __forceinline__ u32x4 get(int nb, int c, int lane) const { return lds[(nb * 4 + c) * 64 + lane]; }
+};
+
+template <bool FP8, int NB, bool QLDS>
+__device__ __forceinline__ void compute_tile(TileRegs<FP8> &T, const QFrag<NB, QLDS> &qf,
                                              SoftmaxState<NB> &st, int tile, int n, int full_lim,
                                              float sc, int lane) {
     const int j = lane >> 4;
@@ -219,24 +219,30 @@ __device__ __forceinline__ void compute_tile(TileRegs<FP8> &T, const u32x4 (&qf)
     // ---- S^T = K Q^T -------------------------------------------------------
     f32x4 s[2][NB];
 #pragma unroll
-    for (int mb = 0; mb < 2; ++mb) {
+    for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb) s[mb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int c = 0; c < 4; ++c) {
-            u32x4 kf;
+    for (int c = 0; c < 4; ++c) {
+        u32x4 kf[2];
+#pragma unroll
+        for (int mb = 0; mb < 2; ++mb) {
             if (FP8) {
                 const u32x4 raw = T.k[mb][c >> 1];
-                kf = (c & 1) ? fp8x8_to_bf16x8(raw.z, raw.w) : fp8x8_to_bf16x8(raw.x, raw.y);
+                kf[mb] = (c & 1) ? fp8x8_to_bf16x8(raw.z, raw.w) : fp8x8_to_bf16x8(raw.x, raw.y);
             } else {
-                kf = T.k[mb][c];
+                kf[mb] = T.k[mb][c];
             }
+        }
 #pragma unroll
-            for (int nb = 0; nb < NB; ++nb) s[mb][nb] = mfma_bf16(kf, qf[nb][c], s[mb][nb]);
+        for (int nb = 0; nb < NB; ++nb) {
+            const u32x4 q = qf.get(nb, c, lane);
+            s[0][nb] = mfma_bf16(kf[0], q, s[0][nb]);
+            s[1][nb] = mfma_bf16(kf[1], q, s[1][nb]);
         }
     }
 
-    // ---- mask, online softmax (base 2) ---------------------------------------
+    // ---- mask, online softmax (base 2, scale folded into the exponent) ------
     // The reference maximum of a row only moves when a tile exceeds it by more
     // than kRescaleLog2 (probabilities stay <= 2^kRescaleLog2), so the
     // accumulator rescale is skipped for almost every tile.
@@ -245,39 +251,37 @@ __device__ __forceinline__ void compute_tile(TileRegs<FP8> &T, const u32x4 (&qf)
     float alpha[NB];
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
-        float x[2][4];
         float mx = -INFINITY;
 #pragma unroll
         for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                float v = s[mb][nb][i] * sc;
-                if (need_mask && key0 + 16 * mb + 4 * i + j >= st.lim[nb]) v = -INFINITY;
-                x[mb][i] = v;
-                mx = fmaxf(mx, v);
+                if (need_mask && key0 + 16 * mb + 4 * i + j >= st.lim[nb]) s[mb][nb][i] = -INFINITY;
+                mx = fmaxf(mx, s[mb][nb][i]);
             }
         mx = fmaxf(mx, __shfl_xor(mx, 16));
         mx = fmaxf(mx, __shfl_xor(mx, 32));
+        mx *= sc;  // sc > 0
         const float mold = st.m[nb];
         const float mnew = mx > mold + kRescaleLog2 ? mx : mold;
         const float msub = mnew == -INFINITY ? 0.f : mnew;
         alpha[nb] = exp2f(mold - msub);  // 1 when unchanged, 0 from -inf
         st.m[nb] = mnew;
+        float p[2][4];
         float psum = 0.f;
 #pragma unroll
         for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                x[mb][i] = exp2f(x[mb][i] - msub);
-                psum += x[mb][i];
+                p[mb][i] = exp2f(fmaf(s[mb][nb][i], sc, -msub));
+                psum += p[mb][i];
             }
         st.l[nb] = st.l[nb] * alpha[nb] + psum;
-        pb[nb].x = pack_bf16x2(x[0][0], x[0][1]);
-        pb[nb].y = pack_bf16x2(x[0][2], x[0][3]);
-        pb[nb].z = pack_bf16x2(x[1][0], x[1][1]);
-        pb[nb].w = pack_bf16x2(x[1][2], x[1][3]);
+        pb[nb].x = pack_bf16x2(p[0][0], p[0][1]);
+        pb[nb].y = pack_bf16x2(p[0][2], p[0][3]);
+        pb[nb].z = pack_bf16x2(p[1][0], p[1][1]);
+        pb[nb].w = pack_bf16x2(p[1][2], p[1][3]);
     }
-
     bool rescale = false;
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) rescale |= alpha[nb] != 1.f;
@@ -324,9 +328,12 @@ __device__ __forceinline__ void compute_tile(TileRegs<FP8> &T, const u32x4 (&qf)
 
 template <bool FP8, int NB, int MODE>
 __global__ __launch_bounds__(256, 1) void mfma_partial_kernel(Problem p, Plan pl) {
+    constexpr bool QLDS = NB > 2;
+    __shared__ u32x4 qlds[QLDS ? kMfmaWavesPerWG * NB * 4 * 64 : 1];
     const int lane = threadIdx.x & 63;
     const int n16 = lane & 15, j = lane >> 4;
-    const int wid = __builtin_amdgcn_readfirstlane(blockIdx.x * kMfmaWavesPerWG + (threadIdx.x >> 6));
+    const int wave = threadIdx.x >> 6;
+    const int wid = __builtin_amdgcn_readfirstlane(blockIdx.x * kMfmaWavesPerWG + wave);
     if (wid >= pl.workers) return;
     const int64_t T = (int64_t)uload(pl.prefix, p.B) * pl.units;
     int64_t pos = worker_begin(wid, T, pl.workers);
@@ -335,6 +342,9 @@ __global__ __launch_bounds__(256, 1) void mfma_partial_kernel(Problem p, Plan pl
     int seg = uload(pl.wstart, 2 * wid);
     int tile = uload(pl.wstart, 2 * wid + 1);
     const int64_t begin = pos;
+
+    QFrag<NB, QLDS> qf;
+    if constexpr (QLDS) qf.lds = qlds + wave * NB * 4 * 64;
 
     while (pos < end) {
         const int b = seg / pl.units;
@@ -368,21 +378,21 @@ __global__ __launch_bounds__(256, 1) void mfma_partial_kernel(Problem p, Plan pl
             a.sink_tok_bytes = p.sink.s_tok * p.sink.elem;
             const int mraw = uload(p.lens, b);
             const int m = mraw < 0 ? 0 : mraw;
-            a.ns = m < p.S ? m : p.S;
+            const int ns = m < p.S ? m : p.S;
+            a.nr = n - ns;
             a.W = p.W;
-            int first = m - p.S - p.W;  // first valid logical ring index
-            first = first < 0 ? 0 : first;
-            int o = 0;
-            if (p.W > 0) {
-                o = uload(p.ring_offset, b) % p.W;
+            int rs = 0;
+            if (p.W > 0 && a.nr < p.W) {  // ring not yet full: start at the oldest valid slot
+                int first = m - p.S - p.W;
+                first = first < 0 ? 0 : first;
+                int o = uload(p.ring_offset, b) % p.W;
                 if (o < 0) o += p.W;
-                o = (n - a.ns == p.W) ? 0 : (o + first % p.W) % p.W;  // full ring: physical order
+                rs = (o + first % p.W) % p.W;
             }
-            a.rs = o;
+            a.rs = rs;  // a full ring is read in physical slot order
         }
 
         // ---- queries: rows 16nb + n16, packed as MFMA B operands ---------------
-        u32x4 qf[NB][4];
         SoftmaxState<NB> st;
         const int full_lim = p.draft ? n : n - p.k;
 #pragma unroll
@@ -396,32 +406,45 @@ __global__ __launch_bounds__(256, 1) void mfma_partial_kernel(Problem p, Plan pl
 #pragma unroll
             for (int c = 0; c < 4; ++c) {
                 const int d0 = FP8 ? 64 * (c >> 1) + 16 * j + 8 * (c & 1) : 32 * c + 8 * j;
-                if (r < p.R)
-                    qf[nb][c] = *reinterpret_cast<const u32x4 *>(p.q + (row_offset(p, b, h, r) + d0) * 2);
-                else
-                    qf[nb][c] = u32x4{0u, 0u, 0u, 0u};
+                u32x4 v = u32x4{0u, 0u, 0u, 0u};
+                if (r < p.R) v = *reinterpret_cast<const u32x4 *>(p.q + (row_offset(p, b, h, r) + d0) * 2);
+                qf.put(nb, c, v, lane);
             }
         }
         float sc = p.sm_scale_log2;
         if (FP8) sc *= uload(p.kv.k_scale, h);
 
-        // ---- tiles [tile, t1): three register buffers, two tiles in flight ----
+        // ---- tiles [tile, t1) ------------------------------------------------------
         if (n > 0) {
-            TileRegs<FP8> A, Bt, C;
             const int last = t1 - 1;
-            load_tile<FP8, MODE>(A, a, tile, lane);
-            load_tile<FP8, MODE>(Bt, a, tile + 1 < last ? tile + 1 : last, lane);
-            int tt = tile;
-            while (true) {
-                load_tile<FP8, MODE>(C, a, tt + 2 < last ? tt + 2 : last, lane);
-                compute_tile<FP8, NB>(A, qf, st, tt, n, full_lim, sc, lane);
-                if (++tt > last) break;
-                load_tile<FP8, MODE>(A, a, tt + 2 < last ? tt + 2 : last, lane);
-                compute_tile<FP8, NB>(Bt, qf, st, tt, n, full_lim, sc, lane);
-                if (++tt > last) break;
-                load_tile<FP8, MODE>(Bt, a, tt + 2 < last ? tt + 2 : last, lane);
-                compute_tile<FP8, NB>(C, qf, st, tt, n, full_lim, sc, lane);
-                if (++tt > last) break;
+            if constexpr (NB <= 2) {  // three register buffers, two tiles in flight
+                TileRegs<FP8> A, Bt, C;
+                load_tile<FP8, MODE>(A, a, tile, lane);
+                load_tile<FP8, MODE>(Bt, a, tile + 1 < last ? tile + 1 : last, lane);
+                int tt = tile;
+                while (true) {
+                    load_tile<FP8, MODE>(C, a, tt + 2 < last ? tt + 2 : last, lane);
+                    compute_tile<FP8, NB>(A, qf, st, tt, n, full_lim, sc, lane);
+                    if (++tt > last) break;
+                    load_tile<FP8, MODE>(A, a, tt + 2 < last ? tt + 2 : last, lane);
+                    compute_tile<FP8, NB>(Bt, qf, st, tt, n, full_lim, sc, lane);
+                    if (++tt > last) break;
+                    load_tile<FP8, MODE>(Bt, a, tt + 2 < last ? tt + 2 : last, lane);
+                    compute_tile<FP8, NB>(C, qf, st, tt, n, full_lim, sc, lane);
+                    if (++tt > last) break;
+                }
+            } else {  // two register buffers, one tile in flight
+                TileRegs<FP8> A, Bt;
+                load_tile<FP8, MODE>(A, a, tile, lane);
+                int tt = tile;
+                while (true) {
+                    load_tile<FP8, MODE>(Bt, a, tt + 1 < last ? tt + 1 : last, lane);
+                    compute_tile<FP8, NB>(A, qf, st, tt, n, full_lim, sc, lane);
+                    if (++tt > last) break;
+                    load_tile<FP8, MODE>(A, a, tt + 1 < last ? tt + 1 : last, lane);
+                    compute_tile<FP8, NB>(Bt, qf, st, tt, n, full_lim, sc, lane);
+                    if (++tt > last) break;
+                }
             }
         }
 

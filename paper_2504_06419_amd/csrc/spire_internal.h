@@ -12,7 +12,11 @@
 //   * a worker that covers a whole segment writes the final rows; otherwise it
 //     writes a partial (normalised output + base-2 log-sum-exp) into slot 2w
 //     (the segment it starts in) or 2w+1 (the segment it ends in), and the
-//     combine kernel merges the partials of each split segment.
+//     combine kernel merges the partials of each split segment.  (Merging
+//     inside the attention kernel by the last worker to finish would need a
+//     device-scope release/acquire per split segment, which on a multi-XCD
+//     MI355X writes back / invalidates L2 and measured slower than a separate
+//     combine launch.)
 #pragma once
 
 #include <hip/hip_runtime.h>
