@@ -170,8 +170,12 @@ int32_t spire_version(void);
 
 /*
  * Kernel selection, process-wide: 0 = automatic (matrix-core kernels where the
- * dtype and shape allow, the generic vector kernel otherwise), 1 = always the
- * generic vector kernel.  Returns SPIRE_ERR_INVALID_ARG for other values.
+ * dtype and shape allow -- LDS-staged for more than 32 rows per KV head,
+ * register-staged otherwise -- and the generic vector kernel for the
+ * rest), 1 = always the generic vector kernel, 2 = prefer the register-staged
+ * matrix-core kernel (it holds at most 32 rows), 3 = prefer the LDS-staged one
+ * (it takes bf16 K/V only above 32 rows), each where its limits allow.
+ * Returns SPIRE_ERR_INVALID_ARG for other values.
  */
 spire_status spire_set_kernel_variant(int32_t variant);
 

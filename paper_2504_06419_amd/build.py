@@ -17,11 +17,20 @@ OUT = os.path.join(HERE, "libspire.so")
 BUILD = os.path.join(HERE, "_build")
 ARCH = "gfx950"
 
-SOURCES = ["spire_abi.hip", "plan_combine.hip", "attn_mfma.hip", "attn_generic.hip"]
+SOURCES = ["spire_abi.hip", "plan_combine.hip", "attn_mfma.hip", "attn_staged.hip",
+           "attn_generic.hip"]
 
 FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
          "-Wall", "-Wno-unused-command-line-argument"]
+
+
+# Matrix-core kernels: select the MFMA forms that accumulate in ordinary VGPRs.
+# With accumulators in AGPRs, every VALU touch of them (the softmax rescale)
+# needs AGPR<->VGPR copies, and the compiler hoists those copies out of the
+# rarely taken rescale branch into every tile.
+MFMA_FLAGS = ["-mllvm", "-amdgpu-mfma-vgpr-form=1"]
+SOURCE_FLAGS = {"attn_mfma.hip": MFMA_FLAGS, "attn_staged.hip": MFMA_FLAGS}
 
 
 def _hipcc():
@@ -35,7 +44,8 @@ def build(verbose: bool = False, extra_flags=()) -> str:
 
     def compile_one(src):
         obj = os.path.join(BUILD, src.replace(".hip", ".o"))
-        cmd = [_hipcc(), *FLAGS, *extra_flags, "-c", os.path.join(CSRC, src), "-o", obj]
+        cmd = [_hipcc(), *FLAGS, *SOURCE_FLAGS.get(src, ()), *extra_flags, "-c",
+               os.path.join(CSRC, src), "-o", obj]
         if verbose:
             print(" ".join(cmd), flush=True)
         r = subprocess.run(cmd, capture_output=True, text=True)

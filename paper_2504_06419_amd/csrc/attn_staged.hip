@@ -1,0 +1,244 @@
+// attn_staged.hip -- LDS-staged matrix-core partial attention (gfx950).
+//
+// Same tile math as attn_mfma.hip (mfma_common.h), but K/V tiles travel
+// HBM -> LDS with the gfx950 global->LDS DMA loads (global_load_lds_dwordx4),
+// which cost no registers while in flight.  That buys two things:
+//   * deep pipelines: a ring of NS tile stages per worker keeps NS-1 tiles in
+//     flight (fp8 tiles are only 8 KB, so register staging cannot hold
+//     enough bytes in flight to cover HBM latency);
+//   * room for many query rows: a worker may be P = 2 waves of one
+//     workgroup that share the stage ring and split the 16-row blocks between
+//     them (3 + 2 blocks for the 72 rows of k = 8 with 8 query heads per KV
+//     head), each keeping its accumulators in registers without spilling.
+//
+// Stage layout (one 32-key tile): the K part is written in MFMA operand order
+// (DMA instruction x, lane L -> the 16 bytes lane L feeds to MFMA call x), so
+// every lane reads back its own slots; the V part is row-major (bf16: DMA lane
+// L of instruction t = the 16 bytes of key 4t + L/16 lane L needs; fp8: 8 whole
+// 128-byte rows per instruction, read back 8 bytes per key per lane).  With
+// P = 2, wave 0 copies K and wave 1 copies V; a workgroup barrier per tile
+// publishes both halves.  The compiler does not track the DMA -> LDS
+// dependency, so the kernel waits on vmcnt explicitly before the barrier.
+#include "mfma_common.h"
+
+namespace spire {
+
+typedef __attribute__((address_space(3))) uint8_t lds_u8;
+
+template <bool FP8> struct Stage {
+    static constexpr int KLOADS = FP8 ? 4 : 8;      // 1 KB DMA instructions for K
+    static constexpr int VLOADS = FP8 ? 4 : 8;      // ... and for V
+    static constexpr int KBYTES = KLOADS * 1024;
+    static constexpr int BYTES = (KLOADS + VLOADS) * 1024;
+};
+
+constexpr int kStagedLdsPerCU = 160 * 1024;
+
+__device__ __forceinline__ void dma16(const uint8_t *g, lds_u8 *l) {
+    __builtin_amdgcn_global_load_lds(reinterpret_cast<const void *>(g),
+                                     reinterpret_cast<__attribute__((address_space(3))) void *>(l), 16, 0, 0);
+}
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+// Copy the K (PART & 1) and/or V (PART & 2) half of tile `tile` into `st`.
+template <bool FP8, int MODE, int PART>
+__device__ __forceinline__ void issue_tile(lds_u8 *st, const SegAddr &a, int tile, int lane) {
+    using G = Stage<FP8>;
+    const int n16 = lane & 15, j = lane >> 4;
+    const int rho = 4 * (n16 & 3) + (n16 >> 2);
+    const int key0 = tile * kMfmaTile;
+    const int64_t g0 = group_base<MODE>(a, key0);
+    const int64_t g1 = group_base<MODE>(a, key0 + 16);
+    const bool fast = MODE == MODE_PAGED || (g0 >= 0 && g1 >= 0);
+    if (PART & 1) {
+        constexpr int NK = FP8 ? 2 : 4;  // 16-byte chunks per key row per lane
+#pragma unroll
+        for (int x = 0; x < G::KLOADS; ++x) {
+            const int mb = x / NK, c = x % NK;
+            const uint8_t *row;
+            if (fast) {
+                row = a.kseq + (mb ? g1 : g0) + (int64_t)rho * a.tok_bytes;
+            } else if (MODE == MODE_DRAFT) {
+                row = draft_row(a, key0 + 16 * mb + rho, false);
+            } else {
+                row = a.kseq + (int64_t)min(key0 + 16 * mb + rho, a.cap - 1) * a.tok_bytes;
+            }
+            dma16(row + 64 * c + 16 * j, st + x * 1024);
+        }
+    }
+    if (PART & 2) {
+#pragma unroll
+        for (int x = 0; x < G::VLOADS; ++x) {
+            // bf16: key 4x + j, bytes 16 n16;  fp8: key 8x + lane/8, bytes 16 (lane % 8)
+            const int kin = FP8 ? 8 * x + (lane >> 3) : 4 * x + j;
+            const int byte = FP8 ? 16 * (lane & 7) : 16 * n16;
+            const uint8_t *row;
+            if (fast) {
+                row = a.vseq + (kin < 16 ? g0 : g1) + (int64_t)(kin & 15) * a.tok_bytes;
+            } else if (MODE == MODE_DRAFT) {
+                row = draft_row(a, key0 + kin, true);
+            } else {
+                row = a.vseq + (int64_t)min(key0 + kin, a.cap - 1) * a.tok_bytes;
+            }
+            dma16(row + byte, st + G::KBYTES + x * 1024);
+        }
+    }
+}
+
+template <bool FP8>
+__device__ __forceinline__ void read_tile(TileRegs<FP8> &T, const lds_u8 *st, int lane) {
+    using G = Stage<FP8>;
+    const int n16 = lane & 15, j = lane >> 4;
+    constexpr int NK = FP8 ? 2 : 4;
+#pragma unroll
+    for (int x = 0; x < G::KLOADS; ++x)
+        T.k[x / NK][x % NK] = *reinterpret_cast<const __attribute__((address_space(3))) u32x4 *>(
+            st + x * 1024 + lane * 16);
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+        if constexpr (FP8)
+            T.v[t] = *reinterpret_cast<const __attribute__((address_space(3))) u32x2 *>(
+                st + G::KBYTES + (4 * t + j) * 128 + 8 * n16);
+        else
+            T.v[t] = *reinterpret_cast<const __attribute__((address_space(3))) u32x4 *>(
+                st + G::KBYTES + t * 1024 + lane * 16);
+    }
+}
+
+// One wave's share of a segment: row blocks rb0 .. rb0+NBW-1 over tiles
+// [t0, t1), stage ring shared by the P waves of the workgroup.
+template <bool FP8, int NBW, int MODE, int P, int NS, bool QL>
+__device__ __forceinline__ void run_segment(const Problem &p, const Plan &pl, lds_u8 *ring,
+                                            u32x4 *qlds, const SegAddr &a, int b, int h, int n,
+                                            int t0, int t1, int rb0, int wave, bool whole,
+                                            int64_t slot, int lane) {
+    using G = Stage<FP8>;
+    constexpr int MINE = P == 1 ? G::KLOADS + G::VLOADS : G::KLOADS;  // == VLOADS
+    QFrag<NBW, QL> qf;
+    if constexpr (QL) qf.lds = qlds;
+    SoftmaxState<NBW, true> st;
+    begin_rows<FP8, NBW, QL, true>(p, b, h, n, rb0, qf, st, lane);
+    const int full_lim = p.draft ? n : n - p.k;
+    float sc = p.sm_scale_log2;
+    if (FP8) sc *= uload(p.kv.k_scale, h);
+
+    if (n > 0) {
+        const int last = t1 - 1;
+        auto issue = [&](int stage, int tile) {
+            lds_u8 *s = ring + stage * G::BYTES;
+            if (P == 1) issue_tile<FP8, MODE, 3>(s, a, tile, lane);
+            else if (wave == 0) issue_tile<FP8, MODE, 1>(s, a, tile, lane);
+            else issue_tile<FP8, MODE, 2>(s, a, tile, lane);
+        };
+#pragma unroll
+        for (int s = 0; s < NS - 1; ++s) issue(s, t0 + s < last ? t0 + s : last);
+        int rd = 0, wr = NS - 1;
+        for (int tt = t0; tt <= last; ++tt) {
+            wait_vmcnt<(NS - 2) * MINE>();  // this wave's part of tile tt has landed
+            __syncthreads();                 // ... and the other waves' parts; tile tt-1 fully read
+            issue(wr, tt + NS - 1 < last ? tt + NS - 1 : last);
+            wr = wr + 1 == NS ? 0 : wr + 1;
+            TileRegs<FP8> T;
+            read_tile<FP8>(T, ring + rd * G::BYTES, lane);
+            rd = rd + 1 == NS ? 0 : rd + 1;
+            compute_tile<FP8, NBW>(T, qf, st, tt, n, full_lim, sc, lane);
+        }
+        wait_vmcnt<0>();  // no copy may still be landing when the next segment reuses the ring
+    }
+    end_rows<FP8, NBW, true>(p, pl, st, b, h, rb0, whole, slot, lane);
+}
+
+template <bool FP8, int NB, int MODE, int P>
+__global__ __launch_bounds__(64 * P, 1) void staged_partial_kernel(Problem p, Plan pl) {
+    using G = Stage<FP8>;
+    constexpr int NB0 = P == 1 ? NB : (NB + 1) / 2;
+    constexpr int NB1 = P == 1 ? 1 : NB / 2;
+    // fp8 stages are half the size of bf16 ones, so parking the query fragments
+    // in LDS (freeing registers for the accumulators) costs fewer of them.
+    constexpr bool QL = FP8;
+    constexpr int QBYTES = QL ? (NB0 + (P == 1 ? 0 : NB1)) * 4 * 64 * 16 : 0;
+    constexpr int LDS = kStagedLdsPerCU / (4 / P);
+    constexpr int NS = (LDS - QBYTES) / G::BYTES;
+    static_assert(NS >= 3, "stage ring too small");
+    __shared__ __attribute__((aligned(1024))) uint8_t smem[NS * G::BYTES + QBYTES];
+    lds_u8 *ring = (lds_u8 *)smem;
+    u32x4 *qsmem = reinterpret_cast<u32x4 *>(smem + NS * G::BYTES);
+
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int wid = blockIdx.x;
+    if (wid >= pl.workers) return;
+    const int64_t T = (int64_t)uload(pl.prefix, p.B) * pl.units;
+    int64_t pos = worker_begin(wid, T, pl.workers);
+    const int64_t end = worker_begin(wid + 1, T, pl.workers);
+    if (pos >= end) return;
+    int seg = uload(pl.wstart, 2 * wid);
+    int tile = uload(pl.wstart, 2 * wid + 1);
+    const int64_t begin = pos;
+
+    while (pos < end) {
+        const int b = seg / pl.units;
+        const int h = seg - b * pl.units;
+        const int tiles_b = uload(pl.prefix, b + 1) - uload(pl.prefix, b);
+        const int64_t left = end - pos;
+        const int t1 = left < (int64_t)(tiles_b - tile) ? tile + (int)left : tiles_b;
+        const int n = uload(pl.nkeys, b);
+        const SegAddr a = make_seg_addr<MODE>(p, b, h, n);
+        const bool whole = (tile == 0 && t1 == tiles_b);
+        const int64_t slot = 2 * (int64_t)wid + (pos == begin ? 0 : 1);
+        __syncthreads();  // every wave is done with the ring of the previous segment
+        if (P == 1 || wave == 0)
+            run_segment<FP8, NB0, MODE, P, NS, QL>(p, pl, ring, qsmem, a, b, h, n, tile, t1, 0, wave,
+                                               whole, slot, lane);
+        else
+            run_segment<FP8, NB1, MODE, P, NS, QL>(p, pl, ring, qsmem + NB0 * 4 * 64, a, b, h, n, tile,
+                                               t1, NB0, wave, whole, slot, lane);
+        pos += t1 - tile;
+        ++seg;
+        tile = 0;
+    }
+}
+
+template <bool FP8, int NB, int P>
+static hipError_t launch_staged_nb(const Problem &p, const Plan &pl, hipStream_t st) {
+    const dim3 grid(pl.workers), block(64 * P);
+    if (p.draft)
+        hipLaunchKernelGGL((staged_partial_kernel<FP8, NB, MODE_DRAFT, P>), grid, block, 0, st, p, pl);
+    else if (p.kv.page_size > 0)
+        hipLaunchKernelGGL((staged_partial_kernel<FP8, NB, MODE_PAGED, P>), grid, block, 0, st, p, pl);
+    else
+        hipLaunchKernelGGL((staged_partial_kernel<FP8, NB, MODE_CONTIG, P>), grid, block, 0, st, p, pl);
+    return hipGetLastError();
+}
+
+template <bool FP8>
+static hipError_t launch_staged_fp(const Problem &p, const Plan &pl, int nb, hipStream_t st) {
+    if constexpr (!FP8) {
+        // a single bf16 worker would get only 2 stages of 16 KB: the register-
+        // staged kernel serves up to 32 rows instead
+        if (nb <= 2) return hipErrorInvalidValue;
+    }
+    switch (nb) {
+    case 1: if constexpr (FP8) return launch_staged_nb<FP8, 1, 1>(p, pl, st); else return hipErrorInvalidValue;
+    case 2: if constexpr (FP8) return launch_staged_nb<FP8, 2, 1>(p, pl, st); else return hipErrorInvalidValue;
+    case 3: return launch_staged_nb<FP8, 3, 2>(p, pl, st);
+    case 4: return launch_staged_nb<FP8, 4, 2>(p, pl, st);
+    case 5: return launch_staged_nb<FP8, 5, 2>(p, pl, st);
+    default: return hipErrorInvalidValue;
+    }
+}
+
+// Waves per worker of the staged kernel for a given number of row blocks.
+int staged_waves(int nb) { return nb <= 2 ? 1 : 2; }
+
+hipError_t launch_staged_partial(const Problem &p, const Plan &pl, int nb, hipStream_t st) {
+    if (p.kv_dtype == SPIRE_FP8_E4M3FN) return launch_staged_fp<true>(p, pl, nb, st);
+    return launch_staged_fp<false>(p, pl, nb, st);
+}
+
+}  // namespace spire

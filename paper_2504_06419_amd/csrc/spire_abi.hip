@@ -182,17 +182,30 @@ spire_status common_checks(const void *q, int q_dtype, int B, int Hq, int Hkv, i
     return SPIRE_OK;
 }
 
+// Kernel family for a matrix-core eligible request: LDS-staged for more than
+// 32 rows (rows split over two waves, deep stage ring), register-staged
+// otherwise; the variant setting can force either.
+bool use_staged(const Problem &p) {
+    const int nb = (p.R + 15) / 16;
+    if (nb > 2) return true;  // the register-staged kernel holds at most 32 rows
+    if (g_variant == 3) return p.kv_dtype == SPIRE_FP8_E4M3FN;
+    return false;  // measured: up to 32 rows the register-staged kernel is faster
+}
+
 spire_status run(Problem &p, bool use_mfma, void *workspace, size_t ws_bytes, hipStream_t stream,
                  int partial_id) {
     int cus = 0;
     if (device_cus(&cus) != 0) return fail(SPIRE_ERR_HIP, "cannot query the current HIP device");
-    const bool mf = use_mfma && g_variant == 0;
+    const bool mf = use_mfma && g_variant != 1;
+    const bool staged = mf && use_staged(p);
+    const int nb = (p.R + 15) / 16;
     Plan pl;
     pl.tile = mf ? kMfmaTile : kGenericTile;
     const int nrb = mf ? 1 : (p.R + kGenericRowBlock - 1) / kGenericRowBlock;
     pl.units = p.Hkv * nrb;
     pl.rows = mf ? p.R : kGenericRowBlock;
-    pl.workers = mf ? mfma_workers(cus) : generic_workers(cus);
+    pl.workers = !mf ? generic_workers(cus)
+                     : (staged ? cus * kMfmaWavesPerWG / staged_waves(nb) : mfma_workers(cus));
     const Layout L = layout(p.B, pl.rows, p.D, pl.workers);
     if (ws_bytes < L.total)
         return fail(SPIRE_ERR_WORKSPACE, "workspace has %zu bytes, needs %zu", ws_bytes, L.total);
@@ -205,12 +218,15 @@ spire_status run(Problem &p, bool use_mfma, void *workspace, size_t ws_bytes, hi
 
     hipError_t e = timed_launch(0, stream, launch_plan, p, pl);
     if (e != hipSuccess) return fail(SPIRE_ERR_HIP, "plan launch: %s", hipGetErrorString(e));
-    if (mf) {
-        const int nb = (p.R + 15) / 16;
+    if (staged) {
+        auto fn = [](const Problem &pp, const Plan &pp2, hipStream_t s) {
+            return launch_staged_partial(pp, pp2, (pp.R + 15) / 16, s);
+        };
+        e = timed_launch(partial_id, stream, fn, p, pl);
+    } else if (mf) {
         auto fn = [](const Problem &pp, const Plan &pp2, hipStream_t s) {
             return launch_mfma_partial(pp, pp2, (pp.R + 15) / 16, s);
         };
-        (void)nb;
         e = timed_launch(partial_id, stream, fn, p, pl);
     } else {
         e = timed_launch(partial_id, stream, launch_generic_partial, p, pl);
@@ -241,7 +257,7 @@ const char *spire_status_string(spire_status s) {
 const char *spire_last_error(void) { return g_err; }
 
 spire_status spire_set_kernel_variant(int32_t variant) {
-    if (variant != 0 && variant != 1) return fail(SPIRE_ERR_INVALID_ARG, "variant must be 0 or 1");
+    if (variant < 0 || variant > 3) return fail(SPIRE_ERR_INVALID_ARG, "variant must be 0..3");
     g_variant = variant;
     return SPIRE_OK;
 }

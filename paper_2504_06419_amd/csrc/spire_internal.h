@@ -132,6 +132,8 @@ __device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
 hipError_t launch_plan(const Problem &p, const Plan &pl, hipStream_t st);
 hipError_t launch_mfma_partial(const Problem &p, const Plan &pl, int nb, hipStream_t st);
 hipError_t launch_generic_partial(const Problem &p, const Plan &pl, hipStream_t st);
+hipError_t launch_staged_partial(const Problem &p, const Plan &pl, int nb, hipStream_t st);
+int staged_waves(int nb);  // waves per worker of the LDS-staged kernel
 hipError_t launch_combine(const Problem &p, const Plan &pl, hipStream_t st);
 
 // MFMA kernel tile size (keys) and its worker count per CU.

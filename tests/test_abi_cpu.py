@@ -132,7 +132,8 @@ def test_draft_rejects_invalid_arguments(kw, status):
 
 def test_kernel_variant_and_sizes():
     L = spire.load()
-    assert L.spire_set_kernel_variant(2) == INVALID
+    assert L.spire_set_kernel_variant(4) == INVALID
+    assert L.spire_set_kernel_variant(-1) == INVALID
     assert L.spire_set_kernel_variant(0) == OK
     assert L.spire_verify_workspace_size(4, 30, 8, 128, 4) == 0
     assert L.spire_draft_workspace_size(4, 32, 0, 128) == 0

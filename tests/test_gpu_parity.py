@@ -19,7 +19,7 @@ DEV = "cuda"
 NW = W.named_workloads()
 
 
-@pytest.fixture(params=[0, 1], ids=["auto", "generic"])
+@pytest.fixture(params=[0, 1, 2, 3], ids=["auto", "generic", "mfma_regs", "mfma_lds"])
 def variant(request):
     spire.set_kernel_variant(request.param)
     yield request.param
