@@ -78,7 +78,8 @@ typedef enum spire_status {
  *   paged (page_size > 0): blk = block_table[b * max_blocks + j / page_size],
  *     t = j % page_size; page ids are clamped to [0, num_blocks).
  * fp8 storage needs per-KV-head dequantisation scales: the value of a stored
- * byte is decode(byte) * k_scale[h] (keys) or * v_scale[h] (values).
+ * byte is decode(byte) * k_scale[h] (keys) or * v_scale[h] (values); the
+ * scales must be finite and > 0 (device data: not checked).
  */
 typedef struct spire_kv {
     const void *k;               /* device */
@@ -115,7 +116,8 @@ size_t spire_verify_workspace_size(int32_t B, int32_t Hq, int32_t Hkv, int32_t D
  *            above the cache capacity are clamped to it.
  *   sizes    B >= 0, Hkv >= 1, Hq % Hkv == 0, D in {64, 128}, 0 <= k <= 15,
  *            (k+1) * Hq / Hkv <= 128.
- *   sm_scale softmax scale (usually 1/sqrt(D)).
+ *   sm_scale softmax scale (usually 1/sqrt(D)); finite and > 0, else
+ *            SPIRE_ERR_INVALID_ARG.
  *   out      [B, k+1, Hq, D] contiguous, out_dtype SPIRE_F32 or SPIRE_BF16.
  *   lse      [B, k+1, Hq] fp32 natural-log sum-exp, or NULL.
  *   workspace >= spire_verify_workspace_size(B, Hq, Hkv, D, k) bytes of device

@@ -16,6 +16,8 @@
 // final normalisation.
 #pragma once
 
+#include <float.h>
+
 #include "spire_internal.h"
 
 namespace spire {
@@ -183,7 +185,8 @@ template <int NB, bool LS> struct SoftmaxState {
     f32x4 acc[8][NB];            // O^T blocks
     f32x4 lsum[LS ? NB : 1];     // LS: row sums (every entry of a block equal)
     float l[LS ? 1 : NB];        // !LS: per-lane partial row sums
-    float m[NB];
+    float msub[NB];              // reference maximum (base 2), 0 while the row has none
+    float thr[NB];               // rescale threshold on raw scores; -inf: no reference yet
     int lim[NB];
 };
 
@@ -252,46 +255,54 @@ __device__ __forceinline__ void compute_tile(TileRegs<FP8> &T, const QFrag<NB, Q
     }
 
     // ---- online softmax (base 2, scale folded into the exponent) ------------
-    // The reference maximum of a row only moves when a tile exceeds it by more
-    // than kRescaleLog2 (probabilities stay <= 2^kRescaleLog2), so the
-    // accumulator rescale is skipped for almost every tile.
-    u32x4 pb[NB];
-    float alpha[NB];
+    // Each row keeps a reference maximum msub that only moves when a score of
+    // the tile exceeds it by more than kRescaleLog2 (probabilities stay below
+    // 2^kRescaleLog2, far inside the bf16/fp32 range).  The common path only
+    // compares lane-local maxima with the row threshold thr = (msub + T) / sc;
+    // the cross-lane row maximum and the accumulator rescale run only when
+    // some row crosses it (a segment's first tile, rare jumps afterwards).
+    float lmax[NB];
+    bool over = false;
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
-        float mx = fmaxf(fmaxf(fmaxf(s[0][nb][0], s[0][nb][1]), fmaxf(s[0][nb][2], s[0][nb][3])),
+        lmax[nb] = fmaxf(fmaxf(fmaxf(s[0][nb][0], s[0][nb][1]), fmaxf(s[0][nb][2], s[0][nb][3])),
                          fmaxf(fmaxf(s[1][nb][0], s[1][nb][1]), fmaxf(s[1][nb][2], s[1][nb][3])));
-        mx = fmaxf(mx, __shfl_xor(mx, 16));
-        mx = fmaxf(mx, __shfl_xor(mx, 32));
-        mx *= sc;  // sc > 0
-        const float mold = st.m[nb];
-        const float mnew = mx > mold + kRescaleLog2 ? mx : mold;
-        const float msub = mnew == -INFINITY ? 0.f : mnew;
-        alpha[nb] = fast_exp2(mold - msub);  // 1 when unchanged, 0 from -inf
-        st.m[nb] = mnew;
+        over |= lmax[nb] > st.thr[nb];
+    }
+    if (__any(over)) {
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) {
+            float mx = fmaxf(lmax[nb], __shfl_xor(lmax[nb], 16));
+            mx = fmaxf(mx, __shfl_xor(mx, 32));
+            mx *= sc;  // sc > 0
+            const float mold = st.thr[nb] == -INFINITY ? -INFINITY : st.msub[nb];
+            const float mnew = mx > mold + kRescaleLog2 ? mx : mold;
+            const float msub = mnew == -INFINITY ? 0.f : mnew;
+            const float alpha = fast_exp2(mold - msub);  // 1 when unchanged, 0 from -inf
+            st.msub[nb] = msub;
+            // finite once a reference exists (-inf marks "none yet")
+            st.thr[nb] = mnew == -INFINITY ? -INFINITY : fmaxf((mnew + kRescaleLog2) / sc, -FLT_MAX);
+#pragma unroll
+            for (int mb = 0; mb < 8; ++mb) st.acc[mb][nb] *= alpha;
+            if constexpr (LS) st.lsum[nb] *= alpha;
+            else st.l[nb] *= alpha;
+        }
+    }
+    u32x4 pb[NB];
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
         float p[2][4];
 #pragma unroll
         for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
-            for (int i = 0; i < 4; ++i) p[mb][i] = fast_exp2(fmaf(s[mb][nb][i], sc, -msub));
+            for (int i = 0; i < 4; ++i) p[mb][i] = fast_exp2(fmaf(s[mb][nb][i], sc, -st.msub[nb]));
         if constexpr (!LS)
-            st.l[nb] = st.l[nb] * alpha[nb] + (((p[0][0] + p[0][1]) + (p[0][2] + p[0][3])) +
-                                               ((p[1][0] + p[1][1]) + (p[1][2] + p[1][3])));
+            st.l[nb] += ((p[0][0] + p[0][1]) + (p[0][2] + p[0][3])) +
+                        ((p[1][0] + p[1][1]) + (p[1][2] + p[1][3]));
         pb[nb].x = pack_bf16x2(p[0][0], p[0][1]);
         pb[nb].y = pack_bf16x2(p[0][2], p[0][3]);
         pb[nb].z = pack_bf16x2(p[1][0], p[1][1]);
         pb[nb].w = pack_bf16x2(p[1][2], p[1][3]);
-    }
-    bool rescale = false;
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb) rescale |= alpha[nb] != 1.f;
-    if (__any(rescale)) {
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb) {
-#pragma unroll
-            for (int mb = 0; mb < 8; ++mb) st.acc[mb][nb] *= alpha[nb];
-            if constexpr (LS) st.lsum[nb] *= alpha[nb];
-        }
     }
 
     // ---- V: keys beyond the segment end are zeroed (storage there may be anything)
@@ -386,7 +397,8 @@ __device__ __forceinline__ void begin_rows(const Problem &p, int b, int h, int n
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
         const int r = 16 * (rb0 + nb) + n16;
-        st.m[nb] = -INFINITY;
+        st.msub[nb] = 0.f;
+        st.thr[nb] = -INFINITY;
         if constexpr (LS) st.lsum[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
         else st.l[nb] = 0.f;
         st.lim[nb] = r < p.R ? visible_limit(p, n, r) : n;
@@ -423,7 +435,7 @@ __device__ __forceinline__ void end_rows(const Problem &p, const Plan &pl, Softm
         const int r = 16 * (rb0 + nb) + n16;
         if (r >= p.R) continue;
         const float inv = l > 0.f ? vs / l : 0.f;
-        const float lse2 = l > 0.f ? st.m[nb] + log2f(l) : -INFINITY;
+        const float lse2 = l > 0.f ? st.msub[nb] + log2f(l) : -INFINITY;
         if (whole) {
             const int64_t off = row_offset(p, b, h, r) + 32 * j;
 #pragma unroll

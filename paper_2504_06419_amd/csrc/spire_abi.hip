@@ -10,6 +10,8 @@
 #include <mutex>
 #include <vector>
 
+#include <cmath>
+
 #include "spire_internal.h"
 
 using namespace spire;
@@ -272,6 +274,13 @@ size_t spire_draft_workspace_size(int32_t B, int32_t Hq, int32_t Hkv, int32_t D)
     return workspace_bytes_for(B, Hq / Hkv, D);
 }
 
+// The kernels take row maxima of raw scores, which needs a positive scale.
+static spire_status check_scale(float sm_scale) {
+    if (!(sm_scale > 0.f) || !std::isfinite(sm_scale))
+        return fail(SPIRE_ERR_INVALID_ARG, "sm_scale must be finite and > 0 (got %g)", (double)sm_scale);
+    return SPIRE_OK;
+}
+
 spire_status spire_verify_attn(const void *q, int32_t q_dtype, const spire_kv *kv,
                                const int32_t *kv_lens, int32_t B, int32_t Hq, int32_t Hkv,
                                int32_t D, int32_t k, float sm_scale, void *out,
@@ -279,6 +288,8 @@ spire_status spire_verify_attn(const void *q, int32_t q_dtype, const spire_kv *k
                                size_t workspace_bytes, hipStream_t stream) {
     g_err[0] = '\0';
     spire_status s = common_checks(q, q_dtype, B, Hq, Hkv, D, k, out, out_dtype, workspace);
+    if (s != SPIRE_OK) return s;
+    s = check_scale(sm_scale);
     if (s != SPIRE_OK) return s;
     s = check_kv(kv, "kv", D, Hkv, true);
     if (s != SPIRE_OK) return s;
@@ -317,6 +328,8 @@ spire_status spire_draft_sparse_attn(const void *q, int32_t q_dtype, const spire
                                      size_t workspace_bytes, hipStream_t stream) {
     g_err[0] = '\0';
     spire_status s = common_checks(q, q_dtype, B, Hq, Hkv, D, 0, out, out_dtype, workspace);
+    if (s != SPIRE_OK) return s;
+    s = check_scale(sm_scale);
     if (s != SPIRE_OK) return s;
     if (S < 0 || W < 0 || (int64_t)S + W < 1)
         return fail(SPIRE_ERR_INVALID_ARG, "need S >= 0, W >= 0, S + W >= 1 (S=%d, W=%d)", S, W);

@@ -67,8 +67,8 @@ def verify(**kw):
     L = spire.load()
     kvp = None if a["kv"] is None else C.byref(a["kv"])
     return L.spire_verify_attn(a["q"], a["q_dtype"], kvp, a["lens"], a["B"], a["Hq"], a["Hkv"],
-                               a["D"], a["k"], 0.1, a["out"], a["out_dtype"], a["lse"], a["ws"],
-                               a["ws_bytes"], None)
+                               a["D"], a["k"], a.get("sm_scale", 0.1), a["out"], a["out_dtype"],
+                               a["lse"], a["ws"], a["ws_bytes"], None)
 
 
 def draft(**kw):
@@ -78,7 +78,8 @@ def draft(**kw):
     L = spire.load()
     return L.spire_draft_sparse_attn(a["q"], a["q_dtype"], C.byref(a["sink"]), C.byref(a["ring"]),
                                      a["lens"], a["offs"], a["B"], a["Hq"], a["Hkv"], a["D"],
-                                     a["S"], a["W"], 0.1, a["out"], spire.F32, None, a["ws"],
+                                     a["S"], a["W"], a.get("sm_scale", 0.1), a["out"], spire.F32,
+                                     None, a["ws"],
                                      1 << 30, None)
 
 
@@ -105,6 +106,10 @@ def draft(**kw):
     (dict(kv=kv(capacity=0)), INVALID),
     (dict(lens=None), INVALID),
     (dict(B=9000), UNSUPPORTED),
+    (dict(sm_scale=0.0), INVALID),                   # kernels need a positive scale
+    (dict(sm_scale=-0.1), INVALID),
+    (dict(sm_scale=float("nan")), INVALID),
+    (dict(sm_scale=float("inf")), INVALID),
 ])
 def test_verify_rejects_invalid_arguments(kw, status):
     assert verify(**kw) == status
@@ -125,6 +130,7 @@ def test_verify_empty_batch_is_a_no_op():
     (dict(lens=None), INVALID),
     (dict(offs=None), INVALID),
     (dict(D=80), UNSUPPORTED),
+    (dict(sm_scale=-1.0), INVALID),
 ])
 def test_draft_rejects_invalid_arguments(kw, status):
     assert draft(**kw) == status

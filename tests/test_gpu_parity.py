@@ -102,6 +102,25 @@ def test_verify_small_shapes(variant, kv_dtype, ps, k, g):
     _check_verify(inp, TOL[kv_dtype])
 
 
+@pytest.mark.parametrize("kv_dtype", ["bf16", "fp8"])
+@pytest.mark.parametrize("k,g", [(1, 4), (8, 8)])
+def test_verify_growing_scores(variant, kv_dtype, k, g):
+    """Key magnitudes that grow 20x along the sequence, plus isolated spikes:
+    every row's running maximum moves many times inside one worker's range,
+    which exercises the rescale path of the online softmax."""
+    banner(f"verify growing scores {kv_dtype} k={k} g={g} variant={variant}")
+    spec = W.VerifySpec(B=3, Hq=2 * g, Hkv=2, D=128, k=k, ctx_lo=2000, ctx_hi=6000,
+                        kv_dtype=kv_dtype)
+    inp = W.make_verify_inputs(spec, 4242 + k + g, device=DEV)
+    kc = inp.k_cache                                     # [B, Hkv, cap, D]
+    cap = kc.shape[2]
+    ramp = torch.linspace(0.25, 5.0, cap, device=DEV).view(1, 1, cap, 1)
+    kf = kc.float() * ramp
+    kf[:, :, 397::811] *= 3.0                           # spikes
+    kc.copy_(kf.clamp(-448.0, 448.0).to(kc.dtype))
+    _check_verify(inp, TOL[kv_dtype])
+
+
 @pytest.mark.parametrize("D", [64, 128])
 def test_verify_fp32_and_head_dims(variant, D):
     banner(f"verify f32 D={D} variant={variant}")
