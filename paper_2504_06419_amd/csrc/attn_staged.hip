@@ -45,6 +45,16 @@ __device__ __forceinline__ void wait_vmcnt() {
     asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
 
+// Workgroup barrier of the stage ring.  __syncthreads() carries a release
+// fence, for which the compiler waits on every outstanding global->LDS copy
+// (vmcnt(0)), draining the whole ring once per tile.  The copies a ring
+// barrier publishes were already waited for (wait_vmcnt); what must also be
+// complete are the LDS reads of the stage about to be overwritten.  The
+// memory clobber keeps the compiler from moving LDS accesses across it.
+__device__ __forceinline__ void ring_barrier() {
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
 // Copy the K (PART & 1) and/or V (PART & 2) half of tile `tile` into `st`.
 template <bool FP8, int MODE, int PART>
 __device__ __forceinline__ void issue_tile(lds_u8 *st, const SegAddr &a, int tile, int lane) {
@@ -140,7 +150,7 @@ __device__ __forceinline__ void run_segment(const Problem &p, const Plan &pl, ld
         int rd = 0, wr = NS - 1;
         for (int tt = t0; tt <= last; ++tt) {
             wait_vmcnt<(NS - 2) * MINE>();  // this wave's part of tile tt has landed
-            __syncthreads();                 // ... and the other waves' parts; tile tt-1 fully read
+            ring_barrier();                  // ... and the other waves' parts; tile tt-1 fully read
             issue(wr, tt + NS - 1 < last ? tt + NS - 1 : last);
             wr = wr + 1 == NS ? 0 : wr + 1;
             TileRegs<FP8> T;
@@ -153,16 +163,21 @@ __device__ __forceinline__ void run_segment(const Problem &p, const Plan &pl, ld
     end_rows<FP8, NBW, true>(p, pl, st, b, h, rb0, whole, slot, lane);
 }
 
-template <bool FP8, int NB, int MODE, int P>
-__global__ __launch_bounds__(64 * P, 1) void staged_partial_kernel(Problem p, Plan pl) {
+// WPS waves per SIMD: with two, one wave's scalar, LDS and matrix-core
+// instructions issue beside the other's vector instructions (a lone wave
+// issues one instruction at a time), at half the registers and LDS each.
+template <bool FP8, int NB, int MODE, int P, int WPS>
+__global__ __launch_bounds__(64 * P, WPS) void staged_partial_kernel(Problem p, Plan pl) {
     using G = Stage<FP8>;
     constexpr int NB0 = P == 1 ? NB : (NB + 1) / 2;
     constexpr int NB1 = P == 1 ? 1 : NB / 2;
-    // fp8 stages are half the size of bf16 ones, so parking the query fragments
-    // in LDS (freeing registers for the accumulators) costs fewer of them.
-    constexpr bool QL = FP8;
-    constexpr int QBYTES = QL ? (NB0 + (P == 1 ? 0 : NB1)) * 4 * 64 * 16 : 0;
-    constexpr int LDS = kStagedLdsPerCU / (4 / P);
+    // Query fragments in LDS free registers for the accumulators.  fp8 stages
+    // are half the size of bf16 ones, so that costs few stages: at one wave
+    // per SIMD both waves park them; at two, only a wave with three blocks.
+    constexpr bool QL0 = FP8 && (WPS == 1 || NB0 > 2);
+    constexpr bool QL1 = FP8 && WPS == 1 && P == 2;
+    constexpr int QBYTES = ((QL0 ? NB0 : 0) + (QL1 ? NB1 : 0)) * 4 * 64 * 16;
+    constexpr int LDS = kStagedLdsPerCU * P / (4 * WPS);  // 4 * WPS / P workgroups per CU
     constexpr int NS = (LDS - QBYTES) / G::BYTES;
     static_assert(NS >= 3, "stage ring too small");
     __shared__ __attribute__((aligned(1024))) uint8_t smem[NS * G::BYTES + QBYTES];
@@ -193,11 +208,11 @@ __global__ __launch_bounds__(64 * P, 1) void staged_partial_kernel(Problem p, Pl
         const int64_t slot = 2 * (int64_t)wid + (pos == begin ? 0 : 1);
         __syncthreads();  // every wave is done with the ring of the previous segment
         if (P == 1 || wave == 0)
-            run_segment<FP8, NB0, MODE, P, NS, QL>(p, pl, ring, qsmem, a, b, h, n, tile, t1, 0, wave,
-                                               whole, slot, lane);
+            run_segment<FP8, NB0, MODE, P, NS, QL0>(p, pl, ring, qsmem, a, b, h, n, tile, t1, 0,
+                                                    wave, whole, slot, lane);
         else
-            run_segment<FP8, NB1, MODE, P, NS, QL>(p, pl, ring, qsmem + NB0 * 4 * 64, a, b, h, n, tile,
-                                               t1, NB0, wave, whole, slot, lane);
+            run_segment<FP8, NB1, MODE, P, NS, QL1>(p, pl, ring, qsmem + (QL0 ? NB0 : 0) * 4 * 64, a,
+                                                    b, h, n, tile, t1, NB0, wave, whole, slot, lane);
         pos += t1 - tile;
         ++seg;
         tile = 0;
@@ -206,13 +221,14 @@ __global__ __launch_bounds__(64 * P, 1) void staged_partial_kernel(Problem p, Pl
 
 template <bool FP8, int NB, int P>
 static hipError_t launch_staged_nb(const Problem &p, const Plan &pl, hipStream_t st) {
+    constexpr int WPS = staged_wps(FP8, NB);
     const dim3 grid(pl.workers), block(64 * P);
     if (p.draft)
-        hipLaunchKernelGGL((staged_partial_kernel<FP8, NB, MODE_DRAFT, P>), grid, block, 0, st, p, pl);
+        hipLaunchKernelGGL((staged_partial_kernel<FP8, NB, MODE_DRAFT, P, WPS>), grid, block, 0, st, p, pl);
     else if (p.kv.page_size > 0)
-        hipLaunchKernelGGL((staged_partial_kernel<FP8, NB, MODE_PAGED, P>), grid, block, 0, st, p, pl);
+        hipLaunchKernelGGL((staged_partial_kernel<FP8, NB, MODE_PAGED, P, WPS>), grid, block, 0, st, p, pl);
     else
-        hipLaunchKernelGGL((staged_partial_kernel<FP8, NB, MODE_CONTIG, P>), grid, block, 0, st, p, pl);
+        hipLaunchKernelGGL((staged_partial_kernel<FP8, NB, MODE_CONTIG, P, WPS>), grid, block, 0, st, p, pl);
     return hipGetLastError();
 }
 
@@ -233,8 +249,9 @@ static hipError_t launch_staged_fp(const Problem &p, const Plan &pl, int nb, hip
     }
 }
 
-// Waves per worker of the staged kernel for a given number of row blocks.
-int staged_waves(int nb) { return nb <= 2 ? 1 : 2; }
+int staged_workers(int cus, int nb, bool fp8) {
+    return cus * 4 * staged_wps(fp8, nb) / staged_waves(nb);
+}
 
 hipError_t launch_staged_partial(const Problem &p, const Plan &pl, int nb, hipStream_t st) {
     if (p.kv_dtype == SPIRE_FP8_E4M3FN) return launch_staged_fp<true>(p, pl, nb, st);

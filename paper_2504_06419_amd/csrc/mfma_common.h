@@ -190,6 +190,18 @@ template <int NB, bool LS> struct SoftmaxState {
     int lim[NB];
 };
 
+// Maximum of 8 scores with the NaN-propagating maximum (v_maximum3_f32): the
+// IEEE-mode fmaxf would first quiet each matrix-core result with an extra
+// instruction.  A NaN score (only from NaN keys inside the visible range)
+// never passes the threshold test.
+__device__ __forceinline__ float max3n(float a, float b, float c) {
+    return __builtin_elementwise_maximum(__builtin_elementwise_maximum(a, b), c);
+}
+__device__ __forceinline__ float max8(f32x4 a, f32x4 b) {
+    return __builtin_elementwise_maximum(max3n(a[0], a[1], a[2]),
+                                         max3n(a[3], b[0], max3n(b[1], b[2], b[3])));
+}
+
 // bf16 1.0 in both halves: the A operand whose product with P^T is the row sum
 constexpr uint32_t kOnesBF16x2 = 0x3F803F80u;
 
@@ -265,8 +277,7 @@ __device__ __forceinline__ void compute_tile(TileRegs<FP8> &T, const QFrag<NB, Q
     bool over = false;
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
-        lmax[nb] = fmaxf(fmaxf(fmaxf(s[0][nb][0], s[0][nb][1]), fmaxf(s[0][nb][2], s[0][nb][3])),
-                         fmaxf(fmaxf(s[1][nb][0], s[1][nb][1]), fmaxf(s[1][nb][2], s[1][nb][3])));
+        lmax[nb] = max8(s[0][nb], s[1][nb]);
         over |= lmax[nb] > st.thr[nb];
     }
     if (__any(over)) {

@@ -207,7 +207,8 @@ spire_status run(Problem &p, bool use_mfma, void *workspace, size_t ws_bytes, hi
     pl.units = p.Hkv * nrb;
     pl.rows = mf ? p.R : kGenericRowBlock;
     pl.workers = !mf ? generic_workers(cus)
-                     : (staged ? cus * kMfmaWavesPerWG / staged_waves(nb) : mfma_workers(cus));
+                     : (staged ? staged_workers(cus, nb, p.kv_dtype == SPIRE_FP8_E4M3FN)
+                               : mfma_workers(cus));
     const Layout L = layout(p.B, pl.rows, p.D, pl.workers);
     if (ws_bytes < L.total)
         return fail(SPIRE_ERR_WORKSPACE, "workspace has %zu bytes, needs %zu", ws_bytes, L.total);

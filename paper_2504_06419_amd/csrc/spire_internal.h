@@ -133,7 +133,12 @@ hipError_t launch_plan(const Problem &p, const Plan &pl, hipStream_t st);
 hipError_t launch_mfma_partial(const Problem &p, const Plan &pl, int nb, hipStream_t st);
 hipError_t launch_generic_partial(const Problem &p, const Plan &pl, hipStream_t st);
 hipError_t launch_staged_partial(const Problem &p, const Plan &pl, int nb, hipStream_t st);
-int staged_waves(int nb);  // waves per worker of the LDS-staged kernel
+// LDS-staged kernel: waves per worker (a workgroup), waves per SIMD, and the
+// workers of a launch (at most 4 per CU, like the register-staged kernel, so
+// one workspace size serves both).
+constexpr int staged_waves(int nb) { return nb <= 2 ? 1 : 2; }
+constexpr int staged_wps(bool fp8, int nb) { return fp8 && nb > 2 ? 2 : 1; }
+int staged_workers(int cus, int nb, bool fp8);
 hipError_t launch_combine(const Problem &p, const Plan &pl, hipStream_t st);
 
 // MFMA kernel tile size (keys) and its worker count per CU.
