@@ -7,6 +7,7 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <algorithm>
 #include <mutex>
 #include <vector>
 
@@ -67,13 +68,22 @@ Layout layout(int64_t B, int64_t rows, int64_t D, int64_t workers) {
     return L;
 }
 
+// One wave per SIMD: measured faster than two for the register-staged kernel
+// (two waves halve the tiles each keeps in flight).
 int mfma_workers(int cus) { return cus * kMfmaWavesPerWG; }
 int generic_workers(int cus) { return cus * kMaxWorkersPerCU; }
 
 size_t workspace_bytes_for(int B, int R, int D) {
     int cus = 0;
     if (device_cus(&cus) != 0) return 0;
-    const Layout a = layout(B, R, D, mfma_workers(cus));
+    // the largest launch of any kernel that may serve R rows, either K/V dtype
+    const int nb = (R + 15) / 16;
+    int w = 0;
+    for (bool fp8 : {false, true}) {
+        w = std::max(w, mfma_workers(cus));
+        w = std::max(w, staged_workers(cus, nb, fp8));
+    }
+    const Layout a = layout(B, R, D, w);
     const Layout b = layout(B, kGenericRowBlock, D, generic_workers(cus));
     return a.total > b.total ? a.total : b.total;
 }
