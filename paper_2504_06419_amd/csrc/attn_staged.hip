@@ -23,7 +23,6 @@
 
 namespace spire {
 
-typedef __attribute__((address_space(3))) uint8_t lds_u8;
 
 template <bool FP8> struct Stage {
     static constexpr int KLOADS = FP8 ? 4 : 8;      // 1 KB DMA instructions for K
@@ -34,16 +33,6 @@ template <bool FP8> struct Stage {
 
 constexpr int kStagedLdsPerCU = 160 * 1024;
 
-__device__ __forceinline__ void dma16(const uint8_t *g, lds_u8 *l) {
-    __builtin_amdgcn_global_load_lds(reinterpret_cast<const void *>(g),
-                                     reinterpret_cast<__attribute__((address_space(3))) void *>(l), 16, 0, 0);
-}
-
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-    static_assert(N >= 0 && N < 64, "vmcnt range");
-    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
-}
 
 // Workgroup barrier of the stage ring.  __syncthreads() carries a release
 // fence, for which the compiler waits on every outstanding global->LDS copy

@@ -30,6 +30,22 @@ typedef __bf16 bf16x2 __attribute__((__vector_size__(4)));
 
 enum { MODE_CONTIG = 0, MODE_PAGED = 1, MODE_DRAFT = 2 };
 
+typedef __attribute__((address_space(3))) uint8_t lds_u8;
+
+// 16 bytes per lane HBM -> LDS (global_load_lds_dwordx4): lane L's bytes land
+// at l + 16 L.  The compiler does not track this LDS write, so readers wait
+// on vmcnt explicitly (wait_vmcnt).
+__device__ __forceinline__ void dma16(const uint8_t *g, lds_u8 *l) {
+    __builtin_amdgcn_global_load_lds(reinterpret_cast<const void *>(g),
+                                     reinterpret_cast<__attribute__((address_space(3))) void *>(l), 16, 0, 0);
+}
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
 constexpr float kRescaleLog2 = 8.f;
 
 __device__ __forceinline__ f32x4 mfma_bf16(u32x4 a, u32x4 b, f32x4 c) {
@@ -79,6 +95,7 @@ struct SegAddr {
     int32_t n;                       // keys of the segment
     int32_t cap;                     // contiguous: rows per sequence
     int32_t ps, num_blocks;          // paged
+    int32_t ps_shift;                // paged: log2(ps) when ps is a power of two, else -1
     int32_t nr, rs, W;               // draft: valid ring slots, first slot, window
 };
 
@@ -106,6 +123,8 @@ __device__ __forceinline__ void load_v_row(TileRegs<FP8> &T, int t, const uint8_
 // Branch-free (selects only), so that loads never sit under divergent control flow.
 __device__ __forceinline__ const uint8_t *draft_row(const SegAddr &a, int j, bool value) {
     j = j < a.n ? j : (a.nr > 0 ? 0 : a.n - 1);
+    // no keys at all (n = 0): ring slot 0 if there is a ring, else sink row 0
+    j = j >= 0 ? j : (a.W > 0 ? 0 : a.nr);
     const bool sink = j >= a.nr;
     int s = a.rs + j;
     s = s >= a.W ? s - a.W : s;
@@ -121,11 +140,22 @@ __device__ __forceinline__ int64_t group_base(const SegAddr &a, int key0) {
     if (MODE == MODE_CONTIG) {
         return key0 + 16 <= a.cap ? (int64_t)key0 * a.tok_bytes : -1;
     } else if (MODE == MODE_PAGED) {
-        const int kk = key0 < a.n ? key0 : a.n - 1;
-        int page = uload(a.table, kk / a.ps);
+        const int kk = key0 < a.n ? key0 : (a.n > 0 ? a.n - 1 : 0);  // n = 0: any valid row
+        const uint32_t u = (uint32_t)kk;
+        uint32_t idx, rin;
+        if (a.ps_shift >= 0) {
+            idx = u >> a.ps_shift;
+            rin = u & (uint32_t)(a.ps - 1);
+        } else {
+            idx = u / (uint32_t)a.ps;
+            rin = u - idx * (uint32_t)a.ps;
+        }
+        int page = uload(a.table, (int64_t)idx);
         page = page < 0 ? 0 : (page >= a.num_blocks ? a.num_blocks - 1 : page);
-        const int row = (kk % a.ps) & ~15;
-        return (int64_t)page * a.blk_bytes + (int64_t)row * a.tok_bytes;
+        // 32-bit products: the host routes only pages under 4 GB whose
+        // ps rows span under 2 GB to these kernels
+        return (int64_t)((uint64_t)(uint32_t)page * (uint32_t)a.blk_bytes) +
+               (int64_t)((rin & ~15u) * (uint32_t)a.tok_bytes);
     } else {
         if (key0 + 16 > a.nr) return -1;
         int s = a.rs + key0;
@@ -369,6 +399,7 @@ __device__ __forceinline__ SegAddr make_seg_addr(const Problem &p, int b, int h,
         a.table = p.kv.block_table + (int64_t)b * p.kv.max_blocks;
         a.blk_bytes = p.kv.s_blk * p.kv.elem;
         a.ps = p.kv.page_size;
+        a.ps_shift = (a.ps & (a.ps - 1)) == 0 ? __builtin_ctz(a.ps) : -1;
         a.num_blocks = p.kv.num_blocks;
     } else {
         const int64_t off = ((int64_t)b * p.kv.s_blk + (int64_t)h * p.kv.s_head) * p.kv.elem;
@@ -399,12 +430,11 @@ __device__ __forceinline__ SegAddr make_seg_addr(const Problem &p, int b, int h,
     return a;
 }
 
-// Reset the softmax state of row blocks rb0 .. rb0+NB-1 and load their queries
-// (rows 16(rb0+nb) + n16) as MFMA B operands.
-template <bool FP8, int NB, bool QLDS, bool LS>
-__device__ __forceinline__ void begin_rows(const Problem &p, int b, int h, int n, int rb0,
-                                           QFrag<NB, QLDS> &qf, SoftmaxState<NB, LS> &st, int lane) {
-    const int n16 = lane & 15, j = lane >> 4;
+// Reset the softmax state of row blocks rb0 .. rb0+NB-1.
+template <int NB, bool LS>
+__device__ __forceinline__ void reset_rows(const Problem &p, int n, int rb0, SoftmaxState<NB, LS> &st,
+                                           int lane) {
+    const int n16 = lane & 15;
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
         const int r = 16 * (rb0 + nb) + n16;
@@ -415,6 +445,18 @@ __device__ __forceinline__ void begin_rows(const Problem &p, int b, int h, int n
         st.lim[nb] = r < p.R ? visible_limit(p, n, r) : n;
 #pragma unroll
         for (int mb = 0; mb < 8; ++mb) st.acc[mb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+}
+
+// Load the queries of row blocks rb0 .. rb0+NB-1 (rows 16(rb0+nb) + n16) of
+// segment (b, h) as MFMA B operands.
+template <bool FP8, int NB, bool QLDS>
+__device__ __forceinline__ void load_rows_q(const Problem &p, int b, int h, int rb0,
+                                            QFrag<NB, QLDS> &qf, int lane) {
+    const int n16 = lane & 15, j = lane >> 4;
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+        const int r = 16 * (rb0 + nb) + n16;
 #pragma unroll
         for (int c = 0; c < 4; ++c) {
             const int d0 = FP8 ? 64 * (c >> 1) + 16 * j + 8 * (c & 1) : 32 * c + 8 * j;
@@ -423,6 +465,13 @@ __device__ __forceinline__ void begin_rows(const Problem &p, int b, int h, int n
             qf.put(nb, c, v, lane);
         }
     }
+}
+
+template <bool FP8, int NB, bool QLDS, bool LS>
+__device__ __forceinline__ void begin_rows(const Problem &p, int b, int h, int n, int rb0,
+                                           QFrag<NB, QLDS> &qf, SoftmaxState<NB, LS> &st, int lane) {
+    reset_rows<NB, LS>(p, n, rb0, st, lane);
+    load_rows_q<FP8, NB, QLDS>(p, b, h, rb0, qf, lane);
 }
 
 // Write the rows of blocks rb0 .. rb0+NB-1: final output + lse when the worker

@@ -325,7 +325,14 @@ spire_status spire_verify_attn(const void *q, int32_t q_dtype, const spire_kv *k
     p.out_dtype = out_dtype;
     p.lse = lse;
 
-    const bool layout_ok = kv->page_size > 0 ? (kv->page_size % 16 == 0) : (kv->capacity >= 1);
+    // paged: 16-key groups never straddle a page, and the matrix-core kernels
+    // form page offsets with 32-bit products
+    const int es = elem_size(kv->dtype);
+    const bool layout_ok =
+        kv->page_size > 0
+            ? (kv->page_size % 16 == 0 && (uint64_t)kv->s_blk * es < (1ull << 32) &&
+               (uint64_t)kv->page_size * kv->s_tok * es < (1ull << 31))
+            : (kv->capacity >= 1);
     const bool mfma = (kv->dtype == SPIRE_BF16 || kv->dtype == SPIRE_FP8_E4M3FN) &&
                       q_dtype == SPIRE_BF16 && D == 128 && p.R <= 80 && layout_ok && rows_aligned(kv);
     return run(p, mfma, workspace, workspace_bytes, stream, 1);
