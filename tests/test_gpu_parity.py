@@ -209,6 +209,21 @@ def test_draft_small_shapes(variant, kv_dtype, S, Wn, lo, hi):
         _check_draft(inp, step, TOL[kv_dtype])
 
 
+@pytest.mark.parametrize("kv_dtype", ["bf16", "fp8"])
+@pytest.mark.parametrize("g", [24, 40, 72])
+def test_draft_group_sizes(variant, kv_dtype, g):
+    """Draft with 17..80 query heads per KV head: two row blocks in the
+    register-staged kernel, three to five in the LDS-staged one (ring wrap,
+    sinks and filling rings on every path)."""
+    banner(f"draft g={g} {kv_dtype} variant={variant}")
+    spec = W.DraftSpec(B=5, Hq=2 * g, Hkv=2, D=128, S=4, W=96, steps=2, ctx_lo=1, ctx_hi=400,
+                       kv_dtype=kv_dtype)
+    inp = W.make_draft_inputs(spec, 3000 + g, device=DEV)
+    for step in range(spec.steps):
+        W.write_step_token(inp, step)
+        _check_draft(inp, step, TOL[kv_dtype])
+
+
 # ---------------------------------------------------------------------------
 # properties
 # ---------------------------------------------------------------------------
