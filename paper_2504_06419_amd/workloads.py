@@ -71,6 +71,21 @@ class DraftSpec:
     log_uniform: bool = True
 
 
+@dataclass
+class TokenSpec:
+    """Token verification after the verify pass: per sequence, the target's
+    k+1 next-token distributions and the draft's k distributions over a
+    vocabulary of V tokens.  Target logits are sigma * N(0,1); draft logits
+    add eps * N(0,1) of mismatch (sigma 4, eps 0.55 accept about 4 of 5 draft
+    tokens, i.e. about 3.4 tokens per round at k = 4, the average generation
+    length the paper reports for SPIRe at L = 512)."""
+    B: int
+    k: int
+    V: int
+    sigma: float = 4.0
+    eps: float = 0.55
+
+
 def named_workloads():
     """The five workloads the library is validated and measured on."""
     return {
@@ -93,6 +108,9 @@ def named_workloads():
                             ctx_lo=2048, ctx_hi=65536, kv_dtype="fp8"),
             verify=VerifySpec(B=512, Hq=64, Hkv=8, D=128, k=8, ctx_lo=2048, ctx_hi=65536,
                               kv_dtype="fp8", page_size=16, spare_pages=64)),
+        # the vocabulary of Llama 3 (the model the paper extrapolates to, Sec. 5.3)
+        "token_verify_B256_k4_V128256": dict(token=TokenSpec(B=256, k=4, V=128256)),
+        "token_verify_B512_k8_V128256": dict(token=TokenSpec(B=512, k=8, V=128256)),
     }
 
 
@@ -456,3 +474,41 @@ def write_step_token(inp: DraftInputs, step: int):
         if is_sink:
             inp.sink_k[b, :, row] = inp.new_k[step, b]
             inp.sink_v[b, :, row] = inp.new_v[step, b]
+
+
+# ----------------------------------------------------------------------------
+# Token verification inputs
+# ----------------------------------------------------------------------------
+@dataclass
+class TokenInputs:
+    spec: TokenSpec
+    p: torch.Tensor          # fp32 [B, k+1, V] target probabilities
+    q: torch.Tensor          # fp32 [B, k, V]   draft probabilities
+    draft: torch.Tensor      # int32 [B, k]     draft tokens, x_i drawn from q_i
+    u_accept: torch.Tensor   # fp32 [B, k]      uniforms of the accept tests
+    u_sample: torch.Tensor   # fp32 [B]         uniform of the emitted token
+
+
+def make_token_inputs(spec: TokenSpec, seed: int, device="cpu", chunk_rows: int = 256) -> TokenInputs:
+    """Seeded distributions, draft tokens and uniforms.  Draw order: target
+    logits, draft-logit noise, draft tokens, accept uniforms, sample uniforms.
+    The softmax here only turns synthetic logits into the probability rows the
+    verification step consumes."""
+    gen = _dev_gen(seed + 15485863, device)
+    B, k, V = spec.B, spec.k, spec.V
+    p = torch.empty((B, k + 1, V), dtype=torch.float32, device=device)
+    q = torch.empty((B, k, V), dtype=torch.float32, device=device)
+    draft = torch.empty((B, k), dtype=torch.int32, device=device)
+    per = max(1, chunk_rows // (k + 1))
+    for s in range(0, B, per):
+        e = min(B, s + per)
+        zt = spec.sigma * _randn((e - s, k + 1, V), gen, device)
+        p[s:e] = torch.softmax(zt, dim=-1)
+        if k > 0:
+            zd = zt[:, :k] + spec.eps * _randn((e - s, k, V), gen, device)
+            q[s:e] = torch.softmax(zd, dim=-1)
+            x = torch.multinomial(q[s:e].reshape(-1, V), 1, generator=gen)
+            draft[s:e] = x.view(e - s, k).to(torch.int32)
+    u_accept = torch.rand((B, k), generator=gen, device=device, dtype=torch.float32)
+    u_sample = torch.rand((B,), generator=gen, device=device, dtype=torch.float32)
+    return TokenInputs(spec=spec, p=p, q=q, draft=draft, u_accept=u_accept, u_sample=u_sample)
