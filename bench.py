@@ -80,7 +80,37 @@ def build_workload(name: str, dev):
     seed = W.MASTER_SEED + W.WORKLOAD_INDEX[name]
     v = W.make_verify_inputs(wl["verify"], seed, device=dev, poison=None) if "verify" in wl else None
     d = W.make_draft_inputs(wl["draft"], seed, device=dev, poison=None) if "draft" in wl else None
-    return wl, v, d
+    t = W.make_token_inputs(wl["token"], seed, device=dev) if "token" in wl else None
+    return wl, v, d, t
+
+
+def token_bytes(t: W.TokenInputs, n_acc) -> int:
+    """Algorithmic bytes of one token verification call, given the accepted
+    counts: the min(n+1, k) accept tests (p and q at the draft token, the
+    token, the uniform), the sampled row of p (and of q for a correction),
+    the sample uniform, and the outputs (n and k+1 tokens)."""
+    s = t.spec
+    total = 0
+    for n in n_acc:
+        tests = min(n + 1, s.k)
+        total += tests * 16 + 4 * s.V * (2 if n < s.k else 1) + 4 + 4 * (s.k + 2)
+    return total
+
+
+def make_token_step(t: W.TokenInputs):
+    """Return (step_fn, bytes_per_step, emitted tokens per step, mean tokens per round)."""
+    s = t.spec
+    ws = spire.workspace(spire.token_verify_workspace_size(s.B, s.k, s.V))
+    n_acc = torch.empty((s.B,), dtype=torch.int32, device=t.p.device)
+    toks = torch.empty((s.B, s.k + 1), dtype=torch.int32, device=t.p.device)
+
+    def step():
+        spire.token_verify(t.p, t.q, t.draft, t.u_accept, t.u_sample, n_acc, toks, ws)
+    step()
+    torch.cuda.synchronize()
+    n = n_acc.cpu().tolist()
+    emitted = sum(x + 1 for x in n)
+    return step, token_bytes(t, n), emitted, emitted / s.B
 
 
 def make_step(v, d):
@@ -119,7 +149,9 @@ def make_step(v, d):
     return step, nbytes, tokens
 
 
-def dominant_bytes(v, d, dominant):
+def dominant_bytes(v, d, dominant, token_step_bytes=None):
+    if dominant == "token_weights":
+        return token_step_bytes
     if dominant == "verify_partial":
         return verify_bytes(v)
     return sum(draft_step_bytes(d, t) for t in range(d.spec.steps)) / d.spec.steps
@@ -174,6 +206,31 @@ def oracle_sample_draft(d, ids, step):
     return dt, nbytes, len(ids)
 
 
+def run_cpu_baseline_token(t: W.TokenInputs, budget_s: float):
+    """The token verification oracle (single-threaded Python + numpy) on whole
+    sequences of the same batch, a seeded order, until the time budget."""
+    from oracle import token_verify as TV
+    s = t.spec
+    g = torch.Generator().manual_seed(0)
+    order = torch.randperm(s.B, generator=g).tolist()
+    total_t, total_b, emitted, used, pos = 0.0, 0, 0, 0, 0
+    while total_t < budget_s and pos < len(order):
+        ids = order[pos:pos + 16]
+        pos += len(ids)
+        idx = torch.tensor(ids, dtype=torch.long, device=t.p.device)
+        args = [x[idx].cpu().numpy() for x in (t.p, t.q, t.draft, t.u_accept, t.u_sample)]
+        t0 = time.perf_counter()
+        n, _ = TV.verify_tokens(*args)
+        total_t += time.perf_counter() - t0
+        total_b += token_bytes(t, n.tolist())
+        emitted += int((n + 1).sum())
+        used += len(ids)
+    return {"value": total_b / total_t / 1e9, "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "sample": f"token verification of {used} of {s.B} sequences (seeded choice)",
+            "seconds": round(total_t, 3), "tokens_per_s": emitted / total_t,
+            "tokens_unit": "emitted tokens/s"}
+
+
 def run_cpu_baseline(v, d, budget_s: float):
     from oracle import oracle as O
     cores = O.threads()
@@ -209,13 +266,14 @@ def run_cpu_baseline(v, d, budget_s: float):
 # ---------------------------------------------------------------------------
 KERNEL_SOURCES = ["paper_2504_06419_amd/csrc/attn_mfma.hip",
                   "paper_2504_06419_amd/csrc/attn_staged.hip",
+                  "paper_2504_06419_amd/csrc/token_verify.hip",
                   "paper_2504_06419_amd/csrc/mfma_common.h",
                   "paper_2504_06419_amd/csrc/spire_internal.h",
                   "paper_2504_06419_amd/build.py"]
 
 
 def kernel_source_hash() -> str:
-    """sha256 over the sources of the attention kernels; recorded HBM traffic is
+    """sha256 over the sources of the measured kernels; recorded HBM traffic is
     reported only while the kernels are the ones the counters were taken on."""
     import hashlib
     h = hashlib.sha256()
@@ -280,8 +338,13 @@ def main():
         return
     spire.load()
     print(f"[bench] building workload {a.workload}", file=sys.stderr, flush=True)
-    wl, v, d = build_workload(a.workload, dev)
-    step, nbytes, tokens = make_step(v, d)
+    wl, v, d, tk = build_workload(a.workload, dev)
+    tok_bytes = None
+    if tk is not None:
+        step, nbytes, tokens, tau = make_token_step(tk)
+        tok_bytes = nbytes
+    else:
+        step, nbytes, tokens = make_step(v, d)
     torch.cuda.synchronize()
 
     print(f"[bench] warmup {a.warmup}", file=sys.stderr, flush=True)
@@ -314,18 +377,23 @@ def main():
         per_kernel.setdefault(name, []).append(t)
     kavg = {k: sum(x) / len(x) for k, x in per_kernel.items()}
     # the dominant kernel is the attention kernel with the most time per step
-    partials = [k for k in ("verify_partial", "draft_partial") if k in per_kernel]
+    partials = [k for k in ("verify_partial", "draft_partial", "token_weights") if k in per_kernel]
     dominant = max(partials, key=lambda k: sum(per_kernel[k]))
     dom_ms = kavg[dominant]
-    dom_bytes = dominant_bytes(v, d, dominant)
+    dom_bytes = dominant_bytes(v, d, dominant, tok_bytes)
     achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
 
     traffic = recorded_traffic(a.traffic_json, a.workload, dominant)
 
     gbs = nbytes / (ms * 1e-3) / 1e9
-    spec = (v or d).spec
-    cfg = {"workload": a.workload, "B": spec.B, "Hq": spec.Hq, "Hkv": spec.Hkv, "D": spec.D,
-           "kv_dtype": spec.kv_dtype}
+    if tk is not None:
+        spec = tk.spec
+        cfg = {"workload": a.workload, "B": spec.B, "k": spec.k, "V": spec.V,
+               "prob_dtype": "f32", "mean_tokens_per_round": round(tau, 4)}
+    else:
+        spec = (v or d).spec
+        cfg = {"workload": a.workload, "B": spec.B, "Hq": spec.Hq, "Hkv": spec.Hkv, "D": spec.D,
+               "kv_dtype": spec.kv_dtype}
     if v is not None:
         cfg.update({"k": v.spec.k, "ctx": [v.spec.ctx_lo, v.spec.ctx_hi],
                     "page_size": v.spec.page_size, "sum_kv_len": int(sum(v.kv_lens.tolist()))})
@@ -334,11 +402,13 @@ def main():
     res = {
         "metric": METRIC, "value": round(gbs, 2), "unit": "GB/s", "n_gpus": 1, "steps": a.steps,
         "warmup": a.warmup, "ms_per_step": round(ms, 5), "higher_is_better": True,
-        "scaling": "weak", "vs_baseline": None, "dtype": spec.kv_dtype, "data": "synthetic",
+        "scaling": "weak", "vs_baseline": None,
+        "dtype": "f32" if tk is not None else spec.kv_dtype, "data": "synthetic",
         "config": cfg,
         "frac_of_hbm_peak": round(gbs / HBM_PEAK_GBS, 4),
         "tokens_per_s": round(tokens / (ms * 1e-3), 1),
-        "tokens_unit": "verified tokens/s" if v is not None else "drafted tokens/s",
+        "tokens_unit": ("emitted tokens/s" if tk is not None else
+                        "verified tokens/s" if v is not None else "drafted tokens/s"),
         "bytes_per_step": nbytes,
         "kernel_ms": {k: round(x, 5) for k, x in kavg.items()},
         "kernel_ms_per_step": {k: round(sum(x) / a.steps, 5) for k, x in per_kernel.items()},
@@ -349,7 +419,8 @@ def main():
     }
     if not a.no_cpu_baseline:
         print(f"[bench] cpu baseline (~{a.cpu_seconds}s)", file=sys.stderr, flush=True)
-        res["cpu_baseline"] = run_cpu_baseline(v, d, a.cpu_seconds)
+        res["cpu_baseline"] = (run_cpu_baseline_token(tk, a.cpu_seconds) if tk is not None
+                               else run_cpu_baseline(v, d, a.cpu_seconds))
     print(json.dumps(res), flush=True)
 
 

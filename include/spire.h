@@ -160,6 +160,48 @@ spire_status spire_draft_sparse_attn(const void *q, int32_t q_dtype, const spire
                                      void *out, int32_t out_dtype, float *lse, void *workspace,
                                      size_t workspace_bytes, hipStream_t stream);
 
+/* Bytes of workspace spire_token_verify needs (0 on invalid sizes). */
+size_t spire_token_verify_workspace_size(int32_t B, int32_t k, int32_t V);
+
+/*
+ * Token verification of one speculation round: the modified rejection
+ * sampling that follows the target's verify pass and makes the accepted
+ * tokens follow the target's distribution (paper Sec. 1 and Sec. 7; Table 1:
+ * a round emits 1..k+1 tokens, 0..k accepted before the first rejection).
+ * For each sequence b:
+ *   n = the number of leading draft tokens x_i (i < k) with
+ *       u_accept[b,i] * q(b,i,x_i) < p(b,i,x_i)   (accept with probability
+ *       min(1, p/q); the product is formed exactly in fp64; a token outside
+ *       [0, V) or a NaN is a rejection);
+ *   the emitted token is drawn with u_sample[b] from the correction
+ *   distribution norm(max(0, p(b,n,.) - q(b,n,.))) when n < k, else from the
+ *   bonus distribution p(b,k,.).
+ * Sampling is an inverse CDF over integer weights W(x) = floor(w(x) * 2^40),
+ * w = clamp(p - q, 0, 1) rounded to fp32 (correction) or clamp(p, 0, 1)
+ * (bonus), NaN weighing 0: with Z = sum W and U = floor(u * 2^24) clamped to
+ * [0, 2^24 - 1], the token is the smallest x whose running weight exceeds
+ * floor(U * Z / 2^24).  A token of zero weight is never drawn; a correction
+ * row with Z = 0 draws from p(b,n,.) instead; a row of p with Z = 0 emits -1.
+ * Results do not depend on the order of any summation (integer arithmetic).
+ *   p_target     [B, k+1, V] fp32 target probabilities; row i scores the
+ *                token after the last accepted token and draft tokens 1..i.
+ *   q_draft      [B, k, V] fp32 draft probabilities (NULL allowed if k == 0).
+ *   draft_tokens [B, k] int32 x_1..x_k;  u_accept [B, k] fp32;  u_sample [B]
+ *                fp32 -- uniforms in [0, 1) supplied by the caller.
+ *   sizes        0 <= B <= 65535, 0 <= k <= 32, 1 <= V <= 2^20.
+ *   n_accepted   [B] int32 out: n.
+ *   out_tokens   [B, k+1] int32 out: the n accepted draft tokens, the emitted
+ *                token, then -1.
+ *   workspace    >= spire_token_verify_workspace_size(B, k, V) bytes, 256-byte
+ *                aligned, contents need no initialisation.
+ * All arrays are contiguous device memory, 4-byte aligned.
+ */
+spire_status spire_token_verify(const float *p_target, const float *q_draft,
+                                const int32_t *draft_tokens, const float *u_accept,
+                                const float *u_sample, int32_t B, int32_t k, int32_t V,
+                                int32_t *n_accepted, int32_t *out_tokens, void *workspace,
+                                size_t workspace_bytes, hipStream_t stream);
+
 /* Human-readable name of a status code (static string, never NULL). */
 const char *spire_status_string(spire_status status);
 
@@ -188,7 +230,8 @@ spire_status spire_set_kernel_variant(int32_t variant);
  * the caller's stream.  spire_timing_collect waits for the recorded events,
  * writes up to `max` (kernel id, milliseconds) pairs in launch order and
  * returns how many it wrote, then forgets them.  Kernel ids: 0 plan,
- * 1 verify partial attention, 2 draft partial attention, 3 combine.  At most
+ * 1 verify partial attention, 2 draft partial attention, 3 combine,
+ * 4 token verification weights, 5 token verification select.  At most
  * 4096 launches are kept between collects (older ones are dropped).
  * spire_timing_enable(0) releases the events.  Not thread-safe.
  */

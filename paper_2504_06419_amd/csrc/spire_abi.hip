@@ -98,19 +98,26 @@ std::vector<TimingRec> g_ev;
 int g_ev_next = 0, g_ev_count = 0;
 bool g_timing = false;
 
-hipError_t timed_launch(int id, hipStream_t st, hipError_t (*fn)(const Problem &, const Plan &, hipStream_t),
-                        const Problem &p, const Plan &pl) {
-    if (!g_timing) return fn(p, pl, st);
+// Record an event pair around one launch (a callable returning hipError_t)
+// on its stream while timing is enabled.
+template <class F>
+hipError_t timed_call(int id, hipStream_t st, F &&launch) {
+    if (!g_timing) return launch();
     TimingRec &r = g_ev[g_ev_next];
     r.id = id;
     hipError_t e = hipEventRecord(r.a, st);
     if (e != hipSuccess) return e;
-    e = fn(p, pl, st);
+    e = launch();
     if (e != hipSuccess) return e;
     e = hipEventRecord(r.b, st);
     g_ev_next = (g_ev_next + 1) % kTimingSlots;
     if (g_ev_count < kTimingSlots) ++g_ev_count;
     return e;
+}
+
+hipError_t timed_launch(int id, hipStream_t st, hipError_t (*fn)(const Problem &, const Plan &, hipStream_t),
+                        const Problem &p, const Plan &pl) {
+    return timed_call(id, st, [&] { return fn(p, pl, st); });
 }
 
 // ---- argument checks --------------------------------------------------------
@@ -387,6 +394,59 @@ spire_status spire_draft_sparse_attn(const void *q, int32_t q_dtype, const spire
                       q_dtype == SPIRE_BF16 && D == 128 && p.R <= 80 && same_scales &&
                       rows_aligned(ring) && rows_aligned(sink);
     return run(p, mfma, workspace, workspace_bytes, stream, 2);
+}
+
+// ---- token verification -------------------------------------------------------
+
+static int token_pieces(int32_t V) { return (V + kTokenPiece - 1) / kTokenPiece; }
+
+size_t spire_token_verify_workspace_size(int32_t B, int32_t k, int32_t V) {
+    if (B < 0 || k < 0 || k > kTokenMaxK || V < 1 || V > kTokenMaxV) return 0;
+    return align256((size_t)B * token_pieces(V) * sizeof(uint64_t)) + align256(4 * (size_t)B + 1);
+}
+
+spire_status spire_token_verify(const float *p_target, const float *q_draft,
+                                const int32_t *draft_tokens, const float *u_accept,
+                                const float *u_sample, int32_t B, int32_t k, int32_t V,
+                                int32_t *n_accepted, int32_t *out_tokens, void *workspace,
+                                size_t workspace_bytes, hipStream_t stream) {
+    g_err[0] = '\0';
+    if (B < 0 || B > 65535) return fail(SPIRE_ERR_UNSUPPORTED, "B must be in [0, 65535] (got %d)", B);
+    if (k < 0 || k > kTokenMaxK) return fail(SPIRE_ERR_UNSUPPORTED, "k must be in [0, %d] (got %d)", kTokenMaxK, k);
+    if (V < 1 || V > kTokenMaxV) return fail(SPIRE_ERR_UNSUPPORTED, "V must be in [1, %d] (got %d)", kTokenMaxV, V);
+    if (B == 0) return SPIRE_OK;
+    if (p_target == nullptr || u_sample == nullptr || n_accepted == nullptr || out_tokens == nullptr)
+        return fail(SPIRE_ERR_INVALID_ARG, "p_target, u_sample, n_accepted or out_tokens is NULL");
+    if (k > 0 && (q_draft == nullptr || draft_tokens == nullptr || u_accept == nullptr))
+        return fail(SPIRE_ERR_INVALID_ARG, "q_draft, draft_tokens or u_accept is NULL with k > 0");
+    const void *ptrs[] = {p_target, q_draft, draft_tokens, u_accept, u_sample, n_accepted, out_tokens};
+    for (const void *ptr : ptrs)
+        if (((uintptr_t)ptr & 3u) != 0) return fail(SPIRE_ERR_INVALID_ARG, "arrays must be 4-byte aligned");
+    const size_t need = spire_token_verify_workspace_size(B, k, V);
+    if (workspace == nullptr) return fail(SPIRE_ERR_WORKSPACE, "workspace is NULL");
+    if (((uintptr_t)workspace & 255u) != 0) return fail(SPIRE_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+    if (workspace_bytes < need)
+        return fail(SPIRE_ERR_WORKSPACE, "workspace has %zu bytes, needs %zu", workspace_bytes, need);
+    TokenProblem t;
+    t.p = p_target;
+    t.q = q_draft;
+    t.draft = draft_tokens;
+    t.u_accept = u_accept;
+    t.u_sample = u_sample;
+    t.B = B;
+    t.k = k;
+    t.V = V;
+    t.npieces = token_pieces(V);
+    t.n_accepted = n_accepted;
+    t.out_tokens = out_tokens;
+    t.piece_sum = static_cast<uint64_t *>(workspace);
+    t.nacc = reinterpret_cast<int32_t *>(static_cast<char *>(workspace) +
+                                         align256((size_t)B * t.npieces * sizeof(uint64_t)));
+    hipError_t e = timed_call(4, stream, [&] { return launch_token_weights(t, stream); });
+    if (e != hipSuccess) return fail(SPIRE_ERR_HIP, "token weights launch: %s", hipGetErrorString(e));
+    e = timed_call(5, stream, [&] { return launch_token_select(t, stream); });
+    if (e != hipSuccess) return fail(SPIRE_ERR_HIP, "token select launch: %s", hipGetErrorString(e));
+    return SPIRE_OK;
 }
 
 spire_status spire_timing_enable(int32_t on) {

@@ -141,6 +141,27 @@ constexpr int staged_wps(bool fp8, int nb) { return fp8 && nb > 2 ? 2 : 1; }
 int staged_workers(int cus, int nb, bool fp8);
 hipError_t launch_combine(const Problem &p, const Plan &pl, hipStream_t st);
 
+// ---- token verification (token_verify.hip) -----------------------------------
+constexpr int kTokenPiece = 2048;    // vocabulary entries per weights wave
+constexpr int kTokenMaxK = 32;
+constexpr int kTokenMaxV = 1 << 20;  // keeps integer weight sums below 2^60
+
+struct TokenProblem {
+    const float *p;          // [B, k+1, V]
+    const float *q;          // [B, k, V] (unused when k == 0)
+    const int32_t *draft;    // [B, k]
+    const float *u_accept;   // [B, k]
+    const float *u_sample;   // [B]
+    int32_t B, k, V;
+    int32_t npieces;         // ceil(V / kTokenPiece)
+    int32_t *n_accepted;     // [B]
+    int32_t *out_tokens;     // [B, k+1]
+    uint64_t *piece_sum;     // workspace [B, npieces]
+    int32_t *nacc;           // workspace [B]: accepted counts (weights -> select)
+};
+hipError_t launch_token_weights(const TokenProblem &t, hipStream_t st);
+hipError_t launch_token_select(const TokenProblem &t, hipStream_t st);
+
 // MFMA kernel tile size (keys) and its worker count per CU.
 constexpr int kMfmaTile = 32;
 constexpr int kMfmaWavesPerWG = 4;

@@ -24,10 +24,12 @@ STATUS = {0: "SPIRE_OK", 1: "SPIRE_ERR_INVALID_ARG", 2: "SPIRE_ERR_UNSUPPORTED",
 
 # exported symbols, in the order include/spire.h declares them
 SYMBOLS = ["spire_verify_workspace_size", "spire_verify_attn", "spire_draft_workspace_size",
-           "spire_draft_sparse_attn", "spire_status_string", "spire_last_error", "spire_version",
-           "spire_set_kernel_variant", "spire_timing_enable", "spire_timing_collect"]
+           "spire_draft_sparse_attn", "spire_token_verify_workspace_size", "spire_token_verify",
+           "spire_status_string", "spire_last_error", "spire_version", "spire_set_kernel_variant",
+           "spire_timing_enable", "spire_timing_collect"]
 
-KERNEL_IDS = {0: "plan", 1: "verify_partial", 2: "draft_partial", 3: "combine"}
+KERNEL_IDS = {0: "plan", 1: "verify_partial", 2: "draft_partial", 3: "combine",
+              4: "token_weights", 5: "token_select"}
 
 
 class SpireError(RuntimeError):
@@ -68,6 +70,10 @@ def load(path: Optional[str] = None):
     L.spire_draft_sparse_attn.restype = C.c_int
     L.spire_draft_sparse_attn.argtypes = [vp, i32, C.POINTER(KV), C.POINTER(KV), vp, vp, i32, i32,
                                           i32, i32, i32, i32, C.c_float, vp, i32, vp, vp, sz, vp]
+    L.spire_token_verify_workspace_size.restype = sz
+    L.spire_token_verify_workspace_size.argtypes = [i32] * 3
+    L.spire_token_verify.restype = C.c_int
+    L.spire_token_verify.argtypes = [vp, vp, vp, vp, vp, i32, i32, i32, vp, vp, vp, sz, vp]
     L.spire_status_string.restype = C.c_char_p
     L.spire_status_string.argtypes = [C.c_int]
     L.spire_last_error.restype = C.c_char_p
@@ -177,6 +183,38 @@ def draft_sparse_attn(q: torch.Tensor, sink: KV, ring: KV, seq_lens: torch.Tenso
                                           D, S, W, float(sm_scale), out.data_ptr(), _DT[out.dtype],
                                           _ptr(lse), ws.data_ptr(), ws.numel(), _stream()))
     return out, lse
+
+
+def token_verify_workspace_size(B, k, V) -> int:
+    return int(load().spire_token_verify_workspace_size(B, k, V))
+
+
+def token_verify(p: torch.Tensor, q: Optional[torch.Tensor], draft: Optional[torch.Tensor],
+                 u_accept: Optional[torch.Tensor], u_sample: torch.Tensor,
+                 n_accepted: Optional[torch.Tensor] = None, tokens: Optional[torch.Tensor] = None,
+                 ws: Optional[torch.Tensor] = None):
+    """spire_token_verify.  p [B, k+1, V] fp32, q [B, k, V] fp32, draft [B, k]
+    int32, u_accept [B, k] fp32, u_sample [B] fp32; returns (n_accepted [B],
+    tokens [B, k+1]) as int32 tensors."""
+    B, kp1, V = p.shape
+    k = kp1 - 1
+    assert p.dtype == torch.float32 and p.is_contiguous() and u_sample.is_contiguous()
+    if k > 0:
+        assert q.shape == (B, k, V) and q.dtype == torch.float32 and q.is_contiguous()
+        assert draft.shape == (B, k) and draft.dtype == torch.int32 and draft.is_contiguous()
+        assert u_accept.shape == (B, k) and u_accept.dtype == torch.float32 and u_accept.is_contiguous()
+    if n_accepted is None:
+        n_accepted = torch.empty((B,), dtype=torch.int32, device=p.device)
+    if tokens is None:
+        tokens = torch.empty((B, kp1), dtype=torch.int32, device=p.device)
+    if ws is None:
+        ws = workspace(token_verify_workspace_size(B, k, V), p.device)
+    _check(load().spire_token_verify(p.data_ptr(), _ptr(q) if k > 0 else None,
+                                     _ptr(draft) if k > 0 else None,
+                                     _ptr(u_accept) if k > 0 else None, u_sample.data_ptr(), B, k,
+                                     V, n_accepted.data_ptr(), tokens.data_ptr(), ws.data_ptr(),
+                                     ws.numel(), _stream()))
+    return n_accepted, tokens
 
 
 def set_kernel_variant(variant: int):

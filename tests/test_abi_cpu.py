@@ -143,3 +143,49 @@ def test_kernel_variant_and_sizes():
     assert L.spire_set_kernel_variant(0) == OK
     assert L.spire_verify_workspace_size(4, 30, 8, 128, 4) == 0
     assert L.spire_draft_workspace_size(4, 32, 0, 128) == 0
+
+
+def token(**kw):
+    a = dict(p=FAKE, q=FAKE, draft=FAKE, ua=FAKE, us=FAKE, B=2, k=4, V=1000, n=FAKE, out=FAKE,
+             ws=FAKE, ws_bytes=1 << 20)
+    a.update(kw)
+    return spire.load().spire_token_verify(a["p"], a["q"], a["draft"], a["ua"], a["us"], a["B"],
+                                           a["k"], a["V"], a["n"], a["out"], a["ws"], a["ws_bytes"],
+                                           None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(B=-1), UNSUPPORTED),
+    (dict(B=70000), UNSUPPORTED),
+    (dict(k=-1), UNSUPPORTED),
+    (dict(k=33), UNSUPPORTED),
+    (dict(V=0), UNSUPPORTED),
+    (dict(V=(1 << 20) + 1), UNSUPPORTED),
+    (dict(p=None), INVALID),
+    (dict(us=None), INVALID),
+    (dict(n=None), INVALID),
+    (dict(out=None), INVALID),
+    (dict(q=None), INVALID),                  # k > 0 needs the draft side
+    (dict(draft=None), INVALID),
+    (dict(ua=None), INVALID),
+    (dict(p=FAKE + 2), INVALID),              # not 4-byte aligned
+    (dict(ws=None), WORKSPACE),
+    (dict(ws=FAKE + 16), WORKSPACE),
+    (dict(ws_bytes=8), WORKSPACE),
+])
+def test_token_verify_rejects_invalid_arguments(kw, status):
+    assert token(**kw) == status
+    assert spire.load().spire_last_error().decode() != ""
+
+
+def test_token_verify_sizes_and_empty_batch():
+    L = spire.load()
+    # one 8-byte sum per 2048-entry piece and sequence plus one 4-byte count per
+    # sequence, each part rounded up to 256 bytes
+    assert L.spire_token_verify_workspace_size(256, 4, 128256) == 256 * 63 * 8 + 1280
+    assert L.spire_token_verify_workspace_size(3, 0, 1) == 512
+    assert L.spire_token_verify_workspace_size(2, 33, 10) == 0
+    assert L.spire_token_verify_workspace_size(2, 4, 0) == 0
+    assert token(B=0, p=None, q=None, draft=None, ua=None, us=None, n=None, out=None, ws=None) == OK
+    # k = 0: the draft side may be absent
+    assert token(k=0, q=None, draft=None, ua=None, ws_bytes=0) == WORKSPACE
