@@ -59,8 +59,10 @@ def threshold(u, Z: int) -> int:
     uf = float(np.float32(u))
     if not uf > 0.0:          # u <= 0 or NaN
         U = 0
-    else:
-        U = min(int(math.floor(uf * float(2 ** U_BITS))), 2 ** U_BITS - 1)
+    elif uf >= 1.0:           # 1, larger values and +inf
+        U = 2 ** U_BITS - 1
+    else:                     # uf * 2^24 is exact; floor(uf * 2^24) <= 2^24 - 1
+        U = int(math.floor(uf * float(2 ** U_BITS)))
     return (U * int(Z)) >> U_BITS     # Python integers: exact
 
 

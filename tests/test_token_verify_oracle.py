@@ -48,6 +48,7 @@ def check_inverse_cdf_hand_values(M):
     assert M.inverse_cdf(W, 0.375) == 3               # T lands exactly on C(1): next token
     assert M.inverse_cdf(W, 1.0 - 2.0 ** -24) == 3
     assert M.inverse_cdf(W, 1.0) == 3                 # clamped uniform
+    assert M.inverse_cdf(W, float("inf")) == 3
     assert M.inverse_cdf(W, float("nan")) == 1        # NaN uniform counts as 0
     assert M.inverse_cdf(np.zeros(4, np.int64), 0.5) == -1
     # correction weights: positive part of p - q, 0.75 - 0.25 = 0.5 exactly
@@ -217,8 +218,7 @@ MUTANTS = {
                                "            if not accept(u_accept[b, n], q[b, n, x], p[b, n, x]):\n"
                                "                n += 1\n                break\n"),
     "shifted_prefix": ("out[b, :n] = draft[b, :n]", "out[b, :n] = np.roll(draft[b], 1)[:n]"),
-    "uniform_not_clamped": ("min(int(math.floor(uf * float(2 ** U_BITS))), 2 ** U_BITS - 1)",
-                            "int(math.floor(uf * float(2 ** U_BITS)))"),
+    "uniform_not_clamped": ("    elif uf >= 1.0:", "    elif uf > 1.0:"),
     "weight_not_clamped_at_one": ("w = np.minimum(w, np.float32(1.0))", "w = w"),
     "no_zero_sum_fallback": ("            if tok < 0:\n                tok = inverse_cdf(weights(p[b, n]), u_sample[b])\n",
                              ""),
