@@ -24,6 +24,7 @@ import os
 import sys
 import time
 
+import numpy as np
 import torch
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
@@ -81,6 +82,8 @@ def build_workload(name: str, dev):
     v = W.make_verify_inputs(wl["verify"], seed, device=dev, poison=None) if "verify" in wl else None
     d = W.make_draft_inputs(wl["draft"], seed, device=dev, poison=None) if "draft" in wl else None
     t = W.make_token_inputs(wl["token"], seed, device=dev) if "token" in wl else None
+    if "kvupd" in wl:
+        t = W.make_kvupdate_inputs(wl["kvupd"], seed, device=dev)
     return wl, v, d, t
 
 
@@ -149,9 +152,52 @@ def make_step(v, d):
     return step, nbytes, tokens
 
 
+def kvupd_launch_bytes(x: W.KvUpdateInputs) -> dict:
+    """Algorithmic bytes per launch of each cache-update kernel: the new K/V
+    read (fp32), the storage rows written, for a draft write also the row it
+    overwrites read and spilled, for a rollback the spilled rows of rejected
+    steps read and written back, plus lengths, offsets and page-table entries."""
+    s = x.spec
+    es = ELEM[s.kv_dtype]
+    row_new, row_st = 2 * s.D * 4, 2 * s.D * es
+    draft = s.B * s.Hkv * (row_new + 3 * row_st) + 8 * s.B
+    append = s.B * (s.k + 1) * (s.Hkv * (row_new + row_st) + 4) + 4 * s.B
+    base = x.base_lens.tolist()
+    rej = 0
+    for b, n in enumerate(x.n_accepted.tolist()):
+        for st in range(n + 1, s.k):
+            p = base[b] + st
+            if p >= 0 and (p < s.S or s.W > 0):
+                rej += 1
+    rollback = rej * s.Hkv * 2 * row_st + 12 * s.B
+    return {"draft_append": draft, "kv_append": append, "draft_rollback": rollback}
+
+
+def make_kvupd_step(x: W.KvUpdateInputs):
+    """One round of cache writes: k draft writes with spills, the target append
+    of the k+1 verified tokens, the rollback of rejected draft writes."""
+    s = x.spec
+    view = spire.kv_view(x.k_cache, x.v_cache, x.block_table, s.page_size, x.k_scale, x.v_scale)
+    sink = spire.kv_view(x.sink_k, x.sink_v, k_scale=x.k_scale, v_scale=x.v_scale)
+    ring = spire.kv_view(x.ring_k, x.ring_v, k_scale=x.k_scale, v_scale=x.v_scale)
+    spk = torch.empty((s.k, s.B, s.Hkv, s.D), dtype=x.ring_k.dtype, device=x.ring_k.device)
+    spv = torch.empty_like(spk)
+    lens = [(x.base_lens + st + 1).to(torch.int32) for st in range(s.k)]
+
+    def step():
+        for st in range(s.k):
+            spire.draft_append(sink, ring, x.draft_k[st], x.draft_v[st], lens[st], x.ring_offset, s.S,
+                               s.W, spk[st], spv[st])
+        spire.kv_append(view, x.new_k, x.new_v, x.base_lens)
+        spire.draft_rollback(sink, ring, spk, spv, x.base_lens, x.n_accepted, x.ring_offset, s.S, s.W)
+    per = kvupd_launch_bytes(x)
+    nbytes = s.k * per["draft_append"] + per["kv_append"] + per["draft_rollback"]
+    return step, nbytes, s.B * (s.k + 1), per, (step, view, sink, ring, spk, spv, lens)
+
+
 def dominant_bytes(v, d, dominant, token_step_bytes=None):
-    if dominant == "token_weights":
-        return token_step_bytes
+    if dominant in ("token_weights", "draft_append", "kv_append", "draft_rollback"):
+        return token_step_bytes[dominant] if isinstance(token_step_bytes, dict) else token_step_bytes
     if dominant == "verify_partial":
         return verify_bytes(v)
     return sum(draft_step_bytes(d, t) for t in range(d.spec.steps)) / d.spec.steps
@@ -231,6 +277,56 @@ def run_cpu_baseline_token(t: W.TokenInputs, budget_s: float):
             "tokens_unit": "emitted tokens/s"}
 
 
+def run_cpu_baseline_kvupd(x: W.KvUpdateInputs, budget_s: float):
+    """The cache-update oracle (single-threaded Python, per element) on whole
+    sequences of the same round, a seeded order, until the time budget."""
+    from oracle import kv_update as KU
+    s = x.spec
+    g = torch.Generator().manual_seed(0)
+    order = torch.randperm(s.B, generator=g).tolist()
+    per = kvupd_launch_bytes(x)
+    per_seq = (s.k * per["draft_append"] + per["kv_append"] + per["draft_rollback"]) / s.B
+    es_np = {"f32": np.float32, "bf16": np.uint16, "fp8": np.uint8}[s.kv_dtype]
+
+    def host(t):
+        t = t.detach().cpu().contiguous()
+        return t.view(torch.uint8).numpy().copy() if s.kv_dtype == "fp8" else (
+            t.view(torch.int16).numpy().view(np.uint16).copy() if s.kv_dtype == "bf16" else t.numpy().copy())
+    ks = None if x.k_scale is None else x.k_scale.cpu().numpy()
+    vs = None if x.v_scale is None else x.v_scale.cpu().numpy()
+    total_t, used, pos = 0.0, 0, 0
+    while total_t < budget_s and pos < len(order):
+        b = order[pos]
+        pos += 1
+        idx = slice(b, b + 1)
+        sk, sv, rk, rv = (host(t[idx]) for t in (x.sink_k, x.sink_v, x.ring_k, x.ring_v))
+        pages = [int(p) for p in x.block_table[b].tolist() if p >= 0]
+        kc, vc = host(x.k_cache[pages]), host(x.v_cache[pages])
+        table = np.full((1, x.block_table.shape[1]), -1, np.int32)
+        for i, p in enumerate(x.block_table[b].tolist()):
+            if p >= 0:
+                table[0, i] = pages.index(p)
+        dk, dv = x.draft_k[:, idx].cpu().numpy(), x.draft_v[:, idx].cpu().numpy()
+        nk, nv = x.new_k[idx].cpu().numpy(), x.new_v[idx].cpu().numpy()
+        base = x.base_lens[idx].cpu().numpy()
+        offs = x.ring_offset[idx].cpu().numpy()
+        nacc = x.n_accepted[idx].cpu().numpy()
+        spk = np.zeros((s.k, 1, s.Hkv, s.D), es_np)
+        spv = np.zeros_like(spk)
+        t0 = time.perf_counter()
+        for st in range(s.k):
+            KU.draft_append(sk, sv, rk, rv, dk[st], dv[st], base + st + 1, offs, s.S, s.W, s.kv_dtype,
+                            ks, vs, spk[st], spv[st])
+        KU.kv_append(kc, vc, nk, nv, base, s.kv_dtype, s.page_size, table, ks, vs)
+        KU.draft_rollback(sk, sv, rk, rv, spk, spv, base, nacc, s.k, offs, s.S, s.W)
+        total_t += time.perf_counter() - t0
+        used += 1
+    return {"value": used * per_seq / total_t / 1e9, "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "sample": f"one round of cache writes for {used} of {s.B} sequences (seeded choice)",
+            "seconds": round(total_t, 3), "tokens_per_s": used * (s.k + 1) / total_t,
+            "tokens_unit": "appended target tokens/s"}
+
+
 def run_cpu_baseline(v, d, budget_s: float):
     from oracle import oracle as O
     cores = O.threads()
@@ -267,6 +363,7 @@ def run_cpu_baseline(v, d, budget_s: float):
 KERNEL_SOURCES = ["paper_2504_06419_amd/csrc/attn_mfma.hip",
                   "paper_2504_06419_amd/csrc/attn_staged.hip",
                   "paper_2504_06419_amd/csrc/token_verify.hip",
+                  "paper_2504_06419_amd/csrc/kv_update.hip",
                   "paper_2504_06419_amd/csrc/mfma_common.h",
                   "paper_2504_06419_amd/csrc/spire_internal.h",
                   "paper_2504_06419_amd/build.py"]
@@ -340,7 +437,10 @@ def main():
     print(f"[bench] building workload {a.workload}", file=sys.stderr, flush=True)
     wl, v, d, tk = build_workload(a.workload, dev)
     tok_bytes = None
-    if tk is not None:
+    is_kvupd = isinstance(tk, W.KvUpdateInputs)
+    if is_kvupd:
+        step, nbytes, tokens, tok_bytes, _keep = make_kvupd_step(tk)
+    elif tk is not None:
         step, nbytes, tokens, tau = make_token_step(tk)
         tok_bytes = nbytes
     else:
@@ -377,7 +477,8 @@ def main():
         per_kernel.setdefault(name, []).append(t)
     kavg = {k: sum(x) / len(x) for k, x in per_kernel.items()}
     # the dominant kernel is the attention kernel with the most time per step
-    partials = [k for k in ("verify_partial", "draft_partial", "token_weights") if k in per_kernel]
+    partials = [k for k in ("verify_partial", "draft_partial", "token_weights", "draft_append",
+                            "kv_append", "draft_rollback") if k in per_kernel]
     dominant = max(partials, key=lambda k: sum(per_kernel[k]))
     dom_ms = kavg[dominant]
     dom_bytes = dominant_bytes(v, d, dominant, tok_bytes)
@@ -386,7 +487,12 @@ def main():
     traffic = recorded_traffic(a.traffic_json, a.workload, dominant)
 
     gbs = nbytes / (ms * 1e-3) / 1e9
-    if tk is not None:
+    if is_kvupd:
+        spec = tk.spec
+        cfg = {"workload": a.workload, "B": spec.B, "Hkv": spec.Hkv, "D": spec.D, "k": spec.k,
+               "S": spec.S, "W": spec.W, "kv_dtype": spec.kv_dtype, "new_dtype": "f32",
+               "page_size": spec.page_size, "ctx": [spec.ctx_lo, spec.ctx_hi]}
+    elif tk is not None:
         spec = tk.spec
         cfg = {"workload": a.workload, "B": spec.B, "k": spec.k, "V": spec.V,
                "prob_dtype": "f32", "mean_tokens_per_round": round(tau, 4)}
@@ -403,11 +509,12 @@ def main():
         "metric": METRIC, "value": round(gbs, 2), "unit": "GB/s", "n_gpus": 1, "steps": a.steps,
         "warmup": a.warmup, "ms_per_step": round(ms, 5), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None,
-        "dtype": "f32" if tk is not None else spec.kv_dtype, "data": "synthetic",
+        "dtype": spec.kv_dtype if is_kvupd else ("f32" if tk is not None else spec.kv_dtype),
+        "data": "synthetic",
         "config": cfg,
         "frac_of_hbm_peak": round(gbs / HBM_PEAK_GBS, 4),
         "tokens_per_s": round(tokens / (ms * 1e-3), 1),
-        "tokens_unit": ("emitted tokens/s" if tk is not None else
+        "tokens_unit": ("appended target tokens/s" if is_kvupd else "emitted tokens/s" if tk is not None else
                         "verified tokens/s" if v is not None else "drafted tokens/s"),
         "bytes_per_step": nbytes,
         "kernel_ms": {k: round(x, 5) for k, x in kavg.items()},
@@ -419,8 +526,12 @@ def main():
     }
     if not a.no_cpu_baseline:
         print(f"[bench] cpu baseline (~{a.cpu_seconds}s)", file=sys.stderr, flush=True)
-        res["cpu_baseline"] = (run_cpu_baseline_token(tk, a.cpu_seconds) if tk is not None
-                               else run_cpu_baseline(v, d, a.cpu_seconds))
+        if is_kvupd:
+            res["cpu_baseline"] = run_cpu_baseline_kvupd(tk, a.cpu_seconds)
+        elif tk is not None:
+            res["cpu_baseline"] = run_cpu_baseline_token(tk, a.cpu_seconds)
+        else:
+            res["cpu_baseline"] = run_cpu_baseline(v, d, a.cpu_seconds)
     print(json.dumps(res), flush=True)
 
 

@@ -202,6 +202,65 @@ spire_status spire_token_verify(const float *p_target, const float *q_draft,
                                 int32_t *n_accepted, int32_t *out_tokens, void *workspace,
                                 size_t workspace_bytes, hipStream_t stream);
 
+/*
+ * Append the K/V of newly verified tokens to the target cache (paper Sec. 2:
+ * the target's forward pass on the k+1 tokens of a round produces their K/V).
+ *   kv        destination view (paged or contiguous, as for spire_verify_attn);
+ *             its k / v storage is WRITTEN (the descriptor's const only means
+ *             the struct is not modified).  fp8 storage needs k_scale / v_scale.
+ *   k_new, v_new  [B, T, Hkv, D] contiguous, new_dtype SPIRE_F32 or SPIRE_BF16.
+ *   positions [B] int32: token t of sequence b goes to cache position
+ *             positions[b] + t (usually the length before the append).  A
+ *             position without storage (negative, at or beyond the contiguous
+ *             capacity, a block beyond max_blocks or a page id outside
+ *             [0, num_blocks)) is skipped, so no value makes the kernel write
+ *             outside the described storage.
+ * Rounding to storage: f32 keeps the value (bf16 input widened exactly);
+ * bf16 rounds to nearest even (NaN stays a quiet NaN); fp8 stores the OCP
+ * e4m3fn code nearest to value / scale[h] (fp32 division; ties to the even
+ * code; magnitudes beyond 448 and infinities saturate to +-448; NaN -> 0x7F).
+ * Pages of the new positions must already be in block_table (page
+ * allocation belongs to the caller).  Sizes: B >= 0, T >= 0, Hkv >= 1,
+ * 1 <= D <= 1024.  No workspace.
+ */
+spire_status spire_kv_append(const spire_kv *kv, const void *k_new, const void *v_new,
+                             int32_t new_dtype, const int32_t *positions, int32_t B, int32_t Hkv,
+                             int32_t D, int32_t T, hipStream_t stream);
+
+/*
+ * One draft step's write into the constant-size StreamingLLM cache (paper
+ * Sec. 3.1): the token at logical position p = seq_lens[b] - 1 is stored in
+ * sink row p (p < S) or ring slot (ring_offset[b] + p - S) mod W, rounded as
+ * for spire_kv_append (sink and ring have one dtype; fp8 uses each view's own
+ * scales).  seq_lens is the m_b of the draft attention that follows.
+ *   k_new, v_new  [B, Hkv, D] contiguous, SPIRE_F32 or SPIRE_BF16.
+ *   spill_k, spill_v  [B, Hkv, D] in the storage dtype, or both NULL: before
+ *             writing, the row being overwritten is copied there (for a full
+ *             ring, p >= S + W, that is the evicted position p - W).  Keep
+ *             one spill area per step of the round for spire_draft_rollback.
+ * A sequence with p < 0, or p >= S without a window (W == 0), writes nothing.
+ */
+spire_status spire_draft_append(const spire_kv *sink, const spire_kv *ring, const void *k_new,
+                                const void *v_new, int32_t new_dtype, const int32_t *seq_lens,
+                                const int32_t *ring_offset, int32_t B, int32_t Hkv, int32_t D,
+                                int32_t S, int32_t W, void *spill_k, void *spill_v,
+                                hipStream_t stream);
+
+/*
+ * Undo the draft writes of rejected steps after token verification.  Step s
+ * of the round (s = 0 .. steps-1) wrote logical position base_lens[b] + s and
+ * kept the overwritten row in spill[s] (spill_k / spill_v are
+ * [steps, B, Hkv, D] in the storage dtype).  With n_accepted[b] = n, steps
+ * s > n wrote rejected tokens: their rows get the spilled bytes back, latest
+ * step first, so afterwards sink and ring hold exactly the bytes that steps
+ * 0 .. n alone would have left (also when steps of one round share a slot).
+ */
+spire_status spire_draft_rollback(const spire_kv *sink, const spire_kv *ring, const void *spill_k,
+                                  const void *spill_v, const int32_t *base_lens,
+                                  const int32_t *n_accepted, int32_t steps,
+                                  const int32_t *ring_offset, int32_t B, int32_t Hkv, int32_t D,
+                                  int32_t S, int32_t W, hipStream_t stream);
+
 /* Human-readable name of a status code (static string, never NULL). */
 const char *spire_status_string(spire_status status);
 
@@ -231,7 +290,8 @@ spire_status spire_set_kernel_variant(int32_t variant);
  * writes up to `max` (kernel id, milliseconds) pairs in launch order and
  * returns how many it wrote, then forgets them.  Kernel ids: 0 plan,
  * 1 verify partial attention, 2 draft partial attention, 3 combine,
- * 4 token verification weights, 5 token verification select.  At most
+ * 4 token verification weights, 5 token verification select, 6 kv append,
+ * 7 draft append, 8 draft rollback.  At most
  * 4096 launches are kept between collects (older ones are dropped).
  * spire_timing_enable(0) releases the events.  Not thread-safe.
  */

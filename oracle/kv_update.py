@@ -171,8 +171,10 @@ def kv_append(k_store, v_store, k_new, v_new, positions, dtype, page_size=0, blo
 
 
 def draft_slot(p: int, S: int, W: int, offset: int):
-    """Where logical position p lives: ('sink', p) for p < S, ('ring', slot)
-    with slot = (offset + p - S) mod W, or None without a window."""
+    """Where logical position p lives: ('sink', p) for 0 <= p < S, ('ring', slot)
+    with slot = (offset + p - S) mod W, or None (negative p, or no window)."""
+    if p < 0:
+        return None
     if p < S:
         return ("sink", p)
     if W <= 0:

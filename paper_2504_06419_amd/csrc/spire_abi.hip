@@ -449,6 +449,109 @@ spire_status spire_token_verify(const float *p_target, const float *q_draft,
     return SPIRE_OK;
 }
 
+// ---- KV cache updates ----------------------------------------------------------
+
+static spire_status check_new(const void *k_new, const void *v_new, int32_t new_dtype, int32_t D) {
+    if (k_new == nullptr || v_new == nullptr) return fail(SPIRE_ERR_INVALID_ARG, "k_new or v_new is NULL");
+    if (new_dtype != SPIRE_F32 && new_dtype != SPIRE_BF16)
+        return fail(SPIRE_ERR_UNSUPPORTED, "new K/V must be F32 or BF16");
+    const uintptr_t al = new_dtype == SPIRE_F32 ? 3u : 1u;
+    if (((uintptr_t)k_new & al) != 0 || ((uintptr_t)v_new & al) != 0)
+        return fail(SPIRE_ERR_INVALID_ARG, "new K/V must be aligned to their element size");
+    if (D < 1 || D > 1024) return fail(SPIRE_ERR_UNSUPPORTED, "D must be in [1, 1024] (got %d)", D);
+    return SPIRE_OK;
+}
+
+static bool elems_aligned(const spire_kv *kv) {
+    const uintptr_t es = (uintptr_t)elem_size(kv->dtype);
+    return es > 0 && ((uintptr_t)kv->k % es) == 0 && ((uintptr_t)kv->v % es) == 0;
+}
+
+spire_status spire_kv_append(const spire_kv *kv, const void *k_new, const void *v_new,
+                             int32_t new_dtype, const int32_t *positions, int32_t B, int32_t Hkv,
+                             int32_t D, int32_t T, hipStream_t stream) {
+    g_err[0] = '\0';
+    if (B < 0 || T < 0 || Hkv < 1) return fail(SPIRE_ERR_INVALID_ARG, "need B >= 0, T >= 0, Hkv >= 1");
+    spire_status s = check_kv(kv, "kv", D, Hkv, true);
+    if (s != SPIRE_OK) return s;
+    if (B == 0 || T == 0) return SPIRE_OK;
+    s = check_new(k_new, v_new, new_dtype, D);
+    if (s != SPIRE_OK) return s;
+    if (positions == nullptr) return fail(SPIRE_ERR_INVALID_ARG, "positions is NULL");
+    if (!elems_aligned(kv)) return fail(SPIRE_ERR_INVALID_ARG, "kv storage not aligned to its element size");
+    if ((int64_t)B * T * Hkv > ((int64_t)1 << 33)) return fail(SPIRE_ERR_UNSUPPORTED, "too many rows");
+    const KvDev d = to_dev(kv);
+    hipError_t e = timed_call(6, stream, [&] {
+        return launch_kv_append(d, k_new, v_new, new_dtype, positions, B, T, Hkv, D, stream);
+    });
+    if (e != hipSuccess) return fail(SPIRE_ERR_HIP, "kv append launch: %s", hipGetErrorString(e));
+    return SPIRE_OK;
+}
+
+static spire_status check_draft_views(const spire_kv *sink, const spire_kv *ring, int32_t S, int32_t W,
+                                      int32_t D, int32_t Hkv) {
+    if (S < 0 || W < 0 || (int64_t)S + W < 1)
+        return fail(SPIRE_ERR_INVALID_ARG, "need S >= 0, W >= 0, S + W >= 1 (S=%d, W=%d)", S, W);
+    spire_status s = check_kv(sink, "sink", D, Hkv, false, S > 0);
+    if (s != SPIRE_OK) return s;
+    s = check_kv(ring, "ring", D, Hkv, false, W > 0);
+    if (s != SPIRE_OK) return s;
+    if (sink->dtype != ring->dtype) return fail(SPIRE_ERR_INVALID_ARG, "sink and ring dtypes differ");
+    if (sink->capacity < S) return fail(SPIRE_ERR_INVALID_ARG, "sink capacity %d < S = %d", sink->capacity, S);
+    if (ring->capacity < W) return fail(SPIRE_ERR_INVALID_ARG, "ring capacity %d < W = %d", ring->capacity, W);
+    if ((S > 0 && !elems_aligned(sink)) || (W > 0 && !elems_aligned(ring)))
+        return fail(SPIRE_ERR_INVALID_ARG, "sink/ring storage not aligned to its element size");
+    return SPIRE_OK;
+}
+
+spire_status spire_draft_append(const spire_kv *sink, const spire_kv *ring, const void *k_new,
+                                const void *v_new, int32_t new_dtype, const int32_t *seq_lens,
+                                const int32_t *ring_offset, int32_t B, int32_t Hkv, int32_t D,
+                                int32_t S, int32_t W, void *spill_k, void *spill_v,
+                                hipStream_t stream) {
+    g_err[0] = '\0';
+    if (B < 0 || Hkv < 1) return fail(SPIRE_ERR_INVALID_ARG, "need B >= 0, Hkv >= 1");
+    spire_status s = check_draft_views(sink, ring, S, W, D, Hkv);
+    if (s != SPIRE_OK) return s;
+    if (B == 0) return SPIRE_OK;
+    s = check_new(k_new, v_new, new_dtype, D);
+    if (s != SPIRE_OK) return s;
+    if (seq_lens == nullptr || ring_offset == nullptr)
+        return fail(SPIRE_ERR_INVALID_ARG, "seq_lens or ring_offset is NULL");
+    if ((spill_k == nullptr) != (spill_v == nullptr))
+        return fail(SPIRE_ERR_INVALID_ARG, "give both spill_k and spill_v, or neither");
+    const KvDev ds = to_dev(sink), dr = to_dev(ring);
+    hipError_t e = timed_call(7, stream, [&] {
+        return launch_draft_append(ds, dr, k_new, v_new, new_dtype, seq_lens, ring_offset, B, Hkv, D, S, W,
+                                   spill_k, spill_v, stream);
+    });
+    if (e != hipSuccess) return fail(SPIRE_ERR_HIP, "draft append launch: %s", hipGetErrorString(e));
+    return SPIRE_OK;
+}
+
+spire_status spire_draft_rollback(const spire_kv *sink, const spire_kv *ring, const void *spill_k,
+                                  const void *spill_v, const int32_t *base_lens,
+                                  const int32_t *n_accepted, int32_t steps,
+                                  const int32_t *ring_offset, int32_t B, int32_t Hkv, int32_t D,
+                                  int32_t S, int32_t W, hipStream_t stream) {
+    g_err[0] = '\0';
+    if (B < 0 || Hkv < 1 || steps < 0) return fail(SPIRE_ERR_INVALID_ARG, "need B >= 0, Hkv >= 1, steps >= 0");
+    if (D < 1 || D > 1024) return fail(SPIRE_ERR_UNSUPPORTED, "D must be in [1, 1024] (got %d)", D);
+    spire_status s = check_draft_views(sink, ring, S, W, D, Hkv);
+    if (s != SPIRE_OK) return s;
+    if (B == 0 || steps == 0) return SPIRE_OK;
+    if (spill_k == nullptr || spill_v == nullptr || base_lens == nullptr || n_accepted == nullptr ||
+        ring_offset == nullptr)
+        return fail(SPIRE_ERR_INVALID_ARG, "spill_k, spill_v, base_lens, n_accepted or ring_offset is NULL");
+    const KvDev ds = to_dev(sink), dr = to_dev(ring);
+    hipError_t e = timed_call(8, stream, [&] {
+        return launch_draft_rollback(ds, dr, spill_k, spill_v, base_lens, n_accepted, steps, ring_offset, B, Hkv,
+                                     D, S, W, stream);
+    });
+    if (e != hipSuccess) return fail(SPIRE_ERR_HIP, "draft rollback launch: %s", hipGetErrorString(e));
+    return SPIRE_OK;
+}
+
 spire_status spire_timing_enable(int32_t on) {
     if (on) {
         if (g_timing) return SPIRE_OK;

@@ -162,6 +162,17 @@ struct TokenProblem {
 hipError_t launch_token_weights(const TokenProblem &t, hipStream_t st);
 hipError_t launch_token_select(const TokenProblem &t, hipStream_t st);
 
+// ---- KV cache updates (kv_update.hip) ------------------------------------------
+hipError_t launch_kv_append(const KvDev &kv, const void *k_new, const void *v_new, int new_dtype,
+                            const int32_t *positions, int B, int T, int Hkv, int D, hipStream_t st);
+hipError_t launch_draft_append(const KvDev &sink, const KvDev &ring, const void *k_new, const void *v_new,
+                               int new_dtype, const int32_t *seq_lens, const int32_t *ring_offset, int B,
+                               int Hkv, int D, int S, int W, void *spill_k, void *spill_v, hipStream_t st);
+hipError_t launch_draft_rollback(const KvDev &sink, const KvDev &ring, const void *spill_k,
+                                 const void *spill_v, const int32_t *base_lens, const int32_t *n_accepted,
+                                 int steps, const int32_t *ring_offset, int B, int Hkv, int D, int S, int W,
+                                 hipStream_t st);
+
 // MFMA kernel tile size (keys) and its worker count per CU.
 constexpr int kMfmaTile = 32;
 constexpr int kMfmaWavesPerWG = 4;

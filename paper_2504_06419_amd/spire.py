@@ -25,11 +25,13 @@ STATUS = {0: "SPIRE_OK", 1: "SPIRE_ERR_INVALID_ARG", 2: "SPIRE_ERR_UNSUPPORTED",
 # exported symbols, in the order include/spire.h declares them
 SYMBOLS = ["spire_verify_workspace_size", "spire_verify_attn", "spire_draft_workspace_size",
            "spire_draft_sparse_attn", "spire_token_verify_workspace_size", "spire_token_verify",
+           "spire_kv_append", "spire_draft_append", "spire_draft_rollback",
            "spire_status_string", "spire_last_error", "spire_version", "spire_set_kernel_variant",
            "spire_timing_enable", "spire_timing_collect"]
 
 KERNEL_IDS = {0: "plan", 1: "verify_partial", 2: "draft_partial", 3: "combine",
-              4: "token_weights", 5: "token_select"}
+              4: "token_weights", 5: "token_select", 6: "kv_append", 7: "draft_append",
+              8: "draft_rollback"}
 
 
 class SpireError(RuntimeError):
@@ -74,6 +76,14 @@ def load(path: Optional[str] = None):
     L.spire_token_verify_workspace_size.argtypes = [i32] * 3
     L.spire_token_verify.restype = C.c_int
     L.spire_token_verify.argtypes = [vp, vp, vp, vp, vp, i32, i32, i32, vp, vp, vp, sz, vp]
+    L.spire_kv_append.restype = C.c_int
+    L.spire_kv_append.argtypes = [C.POINTER(KV), vp, vp, i32, vp, i32, i32, i32, i32, vp]
+    L.spire_draft_append.restype = C.c_int
+    L.spire_draft_append.argtypes = [C.POINTER(KV), C.POINTER(KV), vp, vp, i32, vp, vp, i32, i32, i32,
+                                     i32, i32, vp, vp, vp]
+    L.spire_draft_rollback.restype = C.c_int
+    L.spire_draft_rollback.argtypes = [C.POINTER(KV), C.POINTER(KV), vp, vp, vp, vp, i32, vp, i32, i32,
+                                       i32, i32, i32, vp]
     L.spire_status_string.restype = C.c_char_p
     L.spire_status_string.argtypes = [C.c_int]
     L.spire_last_error.restype = C.c_char_p
@@ -215,6 +225,39 @@ def token_verify(p: torch.Tensor, q: Optional[torch.Tensor], draft: Optional[tor
                                      V, n_accepted.data_ptr(), tokens.data_ptr(), ws.data_ptr(),
                                      ws.numel(), _stream()))
     return n_accepted, tokens
+
+
+def kv_append(kv: KV, k_new: torch.Tensor, v_new: torch.Tensor, positions: torch.Tensor):
+    """spire_kv_append.  k_new / v_new [B, T, Hkv, D] (fp32 or bf16), positions [B] int32."""
+    B, T, Hkv, D = k_new.shape
+    assert v_new.shape == k_new.shape and v_new.dtype == k_new.dtype
+    assert k_new.is_contiguous() and v_new.is_contiguous() and positions.dtype == torch.int32
+    _check(load().spire_kv_append(C.byref(kv), k_new.data_ptr(), v_new.data_ptr(), _DT[k_new.dtype],
+                                  positions.data_ptr(), B, Hkv, D, T, _stream()))
+
+
+def draft_append(sink: KV, ring: KV, k_new: torch.Tensor, v_new: torch.Tensor,
+                 seq_lens: torch.Tensor, ring_offset: torch.Tensor, S: int, W: int,
+                 spill_k: Optional[torch.Tensor] = None, spill_v: Optional[torch.Tensor] = None):
+    """spire_draft_append.  k_new / v_new [B, Hkv, D]; spill [B, Hkv, D] in the storage dtype."""
+    B, Hkv, D = k_new.shape
+    assert v_new.shape == k_new.shape and k_new.is_contiguous() and v_new.is_contiguous()
+    for t in (spill_k, spill_v):
+        assert t is None or (t.is_contiguous() and t.numel() == B * Hkv * D)
+    _check(load().spire_draft_append(C.byref(sink), C.byref(ring), k_new.data_ptr(), v_new.data_ptr(),
+                                     _DT[k_new.dtype], seq_lens.data_ptr(), ring_offset.data_ptr(), B,
+                                     Hkv, D, S, W, _ptr(spill_k), _ptr(spill_v), _stream()))
+
+
+def draft_rollback(sink: KV, ring: KV, spill_k: torch.Tensor, spill_v: torch.Tensor,
+                   base_lens: torch.Tensor, n_accepted: torch.Tensor, ring_offset: torch.Tensor,
+                   S: int, W: int):
+    """spire_draft_rollback.  spill [steps, B, Hkv, D] in the storage dtype."""
+    steps, B, Hkv, D = spill_k.shape
+    assert spill_v.shape == spill_k.shape and spill_k.is_contiguous() and spill_v.is_contiguous()
+    _check(load().spire_draft_rollback(C.byref(sink), C.byref(ring), spill_k.data_ptr(),
+                                       spill_v.data_ptr(), base_lens.data_ptr(), n_accepted.data_ptr(),
+                                       steps, ring_offset.data_ptr(), B, Hkv, D, S, W, _stream()))
 
 
 def set_kernel_variant(variant: int):

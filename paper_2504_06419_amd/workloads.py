@@ -86,6 +86,25 @@ class TokenSpec:
     eps: float = 0.55
 
 
+@dataclass
+class KvUpdateSpec:
+    """Cache writes of one round: k draft steps each store their token in the
+    sink/ring cache (keeping the overwritten row in a spill slot), the target
+    appends the k+1 verified tokens to its paged cache, and the draft writes
+    of rejected steps are rolled back."""
+    B: int
+    Hkv: int
+    D: int
+    k: int
+    S: int
+    W: int
+    ctx_lo: int
+    ctx_hi: int
+    kv_dtype: str = "fp8"
+    page_size: int = 16
+    accept: float = 0.8     # per-token acceptance of the seeded accepted counts
+
+
 def named_workloads():
     """The five workloads the library is validated and measured on."""
     return {
@@ -111,6 +130,8 @@ def named_workloads():
         # the vocabulary of Llama 3 (the model the paper extrapolates to, Sec. 5.3)
         "token_verify_B256_k4_V128256": dict(token=TokenSpec(B=256, k=4, V=128256)),
         "token_verify_B512_k8_V128256": dict(token=TokenSpec(B=512, k=8, V=128256)),
+        "kv_update_round_fp8_B512_k8": dict(kvupd=KvUpdateSpec(B=512, Hkv=8, D=128, k=8, S=4, W=4096,
+                                                                ctx_lo=2048, ctx_hi=65536)),
     }
 
 
@@ -512,3 +533,78 @@ def make_token_inputs(spec: TokenSpec, seed: int, device="cpu", chunk_rows: int 
     u_accept = torch.rand((B, k), generator=gen, device=device, dtype=torch.float32)
     u_sample = torch.rand((B,), generator=gen, device=device, dtype=torch.float32)
     return TokenInputs(spec=spec, p=p, q=q, draft=draft, u_accept=u_accept, u_sample=u_sample)
+
+
+# ----------------------------------------------------------------------------
+# Cache update inputs
+# ----------------------------------------------------------------------------
+@dataclass
+class KvUpdateInputs:
+    spec: KvUpdateSpec
+    base_lens: torch.Tensor     # int32 [B]: L_b, the context before the round
+    k_cache: torch.Tensor       # paged [pages, Hkv, ps, D]: only the pages the append touches
+    v_cache: torch.Tensor
+    block_table: torch.Tensor   # int32 [B, max_blocks] (-1 where no page is mapped)
+    new_k: torch.Tensor         # fp32 [B, k+1, Hkv, D]: the verified tokens' K/V
+    new_v: torch.Tensor
+    sink_k: torch.Tensor        # [B, Hkv, S, D]
+    sink_v: torch.Tensor
+    ring_k: torch.Tensor        # [B, Hkv, W, D]
+    ring_v: torch.Tensor
+    ring_offset: torch.Tensor   # int32 [B]
+    draft_k: torch.Tensor       # fp32 [k, B, Hkv, D]: the draft steps' K/V
+    draft_v: torch.Tensor
+    n_accepted: torch.Tensor    # int32 [B]
+    k_scale: Optional[torch.Tensor]
+    v_scale: Optional[torch.Tensor]
+
+
+def make_kvupdate_inputs(spec: KvUpdateSpec, seed: int, device="cpu") -> KvUpdateInputs:
+    """Seeded state of one round's cache writes.  Draw order: context lengths,
+    ring offsets, scales, page permutation, accepted counts, then (on the
+    device) stored bytes and the new K/V.  Accepted counts follow
+    P(n >= i) = accept^i, truncated at k.  Only the pages holding positions
+    L_b .. L_b + k are mapped, so the target storage stays small while the
+    positions have the workload's lengths."""
+    meta = _cpu_gen(seed)
+    dgen = _dev_gen(seed + 32452843, device)
+    B, Hkv, D, k, S, Wn, ps = spec.B, spec.Hkv, spec.D, spec.k, spec.S, spec.W, spec.page_size
+    base = draw_lengths(meta, B, spec.ctx_lo, spec.ctx_hi, True)
+    offs = torch.randint(0, max(Wn, 1), (B,), generator=meta, dtype=torch.int64)
+    k_scale = v_scale = None
+    if spec.kv_dtype == "fp8":
+        k_scale, v_scale = draw_fp8_scales(meta, Hkv)
+    max_blocks = (max(base) + k + 1 + ps - 1) // ps + 1
+    table = torch.full((B, max_blocks), -1, dtype=torch.int32)
+    need = [list(range(L // ps, (L + k) // ps + 1)) for L in base]
+    pages = sum(len(x) for x in need)
+    perm = torch.randperm(pages, generator=meta)
+    pos = 0
+    for b in range(B):
+        for blk in need[b]:
+            table[b, blk] = int(perm[pos])
+            pos += 1
+    u = torch.rand((B, k), generator=meta, dtype=torch.float64)
+    n_acc = torch.zeros(B, dtype=torch.int32)
+    for b in range(B):
+        n = 0
+        while n < k and float(u[b, n]) < spec.accept:
+            n += 1
+        n_acc[b] = n
+    kc = _fill_random((pages, Hkv, ps, D), spec.kv_dtype, dgen, device, k_scale, 1)
+    vc = _fill_random((pages, Hkv, ps, D), spec.kv_dtype, dgen, device, v_scale, 1)
+    sink_k = _fill_random((B, Hkv, S, D), spec.kv_dtype, dgen, device, k_scale, 1)
+    sink_v = _fill_random((B, Hkv, S, D), spec.kv_dtype, dgen, device, v_scale, 1)
+    ring_k = _fill_random((B, Hkv, Wn, D), spec.kv_dtype, dgen, device, k_scale, 1)
+    ring_v = _fill_random((B, Hkv, Wn, D), spec.kv_dtype, dgen, device, v_scale, 1)
+    new_k = _randn((B, k + 1, Hkv, D), dgen, device)
+    new_v = _randn((B, k + 1, Hkv, D), dgen, device)
+    draft_k = _randn((k, B, Hkv, D), dgen, device)
+    draft_v = _randn((k, B, Hkv, D), dgen, device)
+    dev = lambda t: None if t is None else t.to(device)
+    return KvUpdateInputs(spec=spec, base_lens=torch.tensor(base, dtype=torch.int32, device=device),
+                          k_cache=kc, v_cache=vc, block_table=table.to(device), new_k=new_k,
+                          new_v=new_v, sink_k=sink_k, sink_v=sink_v, ring_k=ring_k, ring_v=ring_v,
+                          ring_offset=offs.to(torch.int32).to(device), draft_k=draft_k,
+                          draft_v=draft_v, n_accepted=n_acc.to(device), k_scale=dev(k_scale),
+                          v_scale=dev(v_scale))

@@ -189,3 +189,85 @@ def test_token_verify_sizes_and_empty_batch():
     assert token(B=0, p=None, q=None, draft=None, ua=None, us=None, n=None, out=None, ws=None) == OK
     # k = 0: the draft side may be absent
     assert token(k=0, q=None, draft=None, ua=None, ws_bytes=0) == WORKSPACE
+
+
+def _append(**kw):
+    a = dict(kv=kv(), k=FAKE, v=FAKE, dt=spire.F32, pos=FAKE, B=2, Hkv=8, D=128, T=5)
+    a.update(kw)
+    return spire.load().spire_kv_append(C.byref(a["kv"]), a["k"], a["v"], a["dt"], a["pos"], a["B"],
+                                        a["Hkv"], a["D"], a["T"], None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(B=-1), INVALID),
+    (dict(T=-1), INVALID),
+    (dict(Hkv=0), INVALID),
+    (dict(k=None), INVALID),
+    (dict(pos=None), INVALID),
+    (dict(dt=spire.FP8), UNSUPPORTED),               # new K/V must be f32 or bf16
+    (dict(D=0), UNSUPPORTED),
+    (dict(D=2000), UNSUPPORTED),
+    (dict(k=FAKE + 2), INVALID),                      # f32 input not 4-byte aligned
+    (dict(kv=kv(dtype=spire.FP8)), INVALID),          # fp8 storage without scales
+    (dict(kv=kv(page_size=16)), INVALID),             # paged without a block table
+    (dict(kv=kv(reserved=1)), INVALID),
+])
+def test_kv_append_rejects_invalid_arguments(kw, status):
+    assert _append(**kw) == status
+    assert spire.load().spire_last_error().decode() != ""
+
+
+def test_kv_append_empty_is_a_no_op():
+    assert _append(B=0, k=None, v=None, pos=None) == OK
+    assert _append(T=0, k=None, v=None, pos=None) == OK
+
+
+def _dappend(**kw):
+    a = dict(sink=kv(capacity=4), ring=kv(capacity=64), k=FAKE, v=FAKE, dt=spire.BF16, lens=FAKE,
+             offs=FAKE, B=2, Hkv=8, D=128, S=4, W=64, sk=None, sv=None)
+    a.update(kw)
+    return spire.load().spire_draft_append(C.byref(a["sink"]), C.byref(a["ring"]), a["k"], a["v"],
+                                           a["dt"], a["lens"], a["offs"], a["B"], a["Hkv"], a["D"],
+                                           a["S"], a["W"], a["sk"], a["sv"], None)
+
+
+def _rollback(**kw):
+    a = dict(sink=kv(capacity=4), ring=kv(capacity=64), sk=FAKE, sv=FAKE, base=FAKE, n=FAKE, steps=4,
+             offs=FAKE, B=2, Hkv=8, D=128, S=4, W=64)
+    a.update(kw)
+    return spire.load().spire_draft_rollback(C.byref(a["sink"]), C.byref(a["ring"]), a["sk"], a["sv"],
+                                             a["base"], a["n"], a["steps"], a["offs"], a["B"],
+                                             a["Hkv"], a["D"], a["S"], a["W"], None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(S=0, W=0), INVALID),
+    (dict(S=8), INVALID),                             # sink capacity 4 < S
+    (dict(W=128), INVALID),                           # ring capacity 64 < W
+    (dict(sink=kv(dtype=spire.F32, capacity=4)), INVALID),
+    (dict(ring=kv(page_size=16, table=FAKE)), UNSUPPORTED),
+    (dict(lens=None), INVALID),
+    (dict(offs=None), INVALID),
+    (dict(k=None), INVALID),
+    (dict(sk=FAKE), INVALID),                         # spill_k without spill_v
+    (dict(dt=7), UNSUPPORTED),
+])
+def test_draft_append_rejects_invalid_arguments(kw, status):
+    assert _dappend(**kw) == status
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(steps=-1), INVALID),
+    (dict(sk=None), INVALID),
+    (dict(base=None), INVALID),
+    (dict(n=None), INVALID),
+    (dict(D=0), UNSUPPORTED),
+    (dict(S=-1), INVALID),
+])
+def test_draft_rollback_rejects_invalid_arguments(kw, status):
+    assert _rollback(**kw) == status
+
+
+def test_draft_updates_empty_are_no_ops():
+    assert _dappend(B=0, k=None, v=None, lens=None, offs=None) == OK
+    assert _rollback(steps=0, sk=None, sv=None, base=None, n=None, offs=None) == OK
