@@ -405,6 +405,55 @@ def recorded_traffic(path: str, workload: str, kernel: str):
     return ent.get("bytes_per_launch")
 
 
+def perf_model_section(v: W.VerifyInputs, d: W.DraftInputs, reps: int) -> dict:
+    """The paper's iteration time multiplier dt = (k t_draft + t_verify) / t_target
+    for the attention of this round, measured (one draft call averaged over the
+    k steps, the verify call, and a target decode: the verify entry point with
+    k = 0 over the same caches, L_b + 1 keys) and modeled (each pass costs
+    max(FLOPs, KV bytes * HOI), HOI = 2.5 PFLOP/s bf16 matrix peak / 8 TB/s,
+    the kernels computing in bf16)."""
+    from paper_2504_06419_amd import perf_model as PM
+    vs, ds = v.spec, d.spec
+    kv = spire.kv_view(v.k_cache, v.v_cache, v.block_table, v.page_size, v.k_scale, v.v_scale)
+    sink = spire.kv_view(d.sink_k, d.sink_v, k_scale=d.k_scale, v_scale=d.v_scale)
+    ring = spire.kv_view(d.ring_k, d.ring_v, k_scale=d.k_scale, v_scale=d.v_scale)
+    q0 = v.q[:, :1].contiguous()
+    lens0 = (v.kv_lens - vs.k).to(torch.int32)
+    ws_t = spire.workspace(spire.verify_workspace_size(vs.B, vs.Hq, vs.Hkv, vs.D, 0))
+    ws_v = spire.workspace(spire.verify_workspace_size(vs.B, vs.Hq, vs.Hkv, vs.D, vs.k))
+    ws_d = spire.workspace(spire.draft_workspace_size(ds.B, ds.Hq, ds.Hkv, ds.D))
+    qs = [d.q[t].contiguous() for t in range(ds.steps)]
+    dl = [d.seq_lens(t) for t in range(ds.steps)]
+
+    def draft_all():
+        for t in range(ds.steps):
+            spire.draft_sparse_attn(qs[t], sink, ring, dl[t], d.ring_offset, ds.S, ds.W, d.sm_scale,
+                                    ds.Hkv, ws=ws_d)
+
+    def timed(fn, n):
+        fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(n):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / n
+
+    t_draft = timed(draft_all, reps) / ds.steps
+    t_verify = timed(lambda: spire.verify_attn(v.q, kv, v.kv_lens, vs.Hkv, vs.k, v.sm_scale, ws=ws_v), reps)
+    t_target = timed(lambda: spire.verify_attn(q0, kv, lens0, vs.Hkv, 0, v.sm_scale, ws=ws_t), reps)
+    hoi = PM.hoi(PM.PEAK_FLOPS["bf16"], PM.HBM_BYTES_PER_S)
+    dt_model = PM.attention_dt(v.context_lens, vs.k, vs.Hq, vs.Hkv, vs.D, ds.S, ds.W,
+                               ELEM[vs.kv_dtype], hoi)
+    return {"t_draft_ms": round(t_draft, 5), "t_verify_ms": round(t_verify, 5),
+            "t_target_ms": round(t_target, 5), "hoi_flop_per_byte": hoi,
+            "dt_measured": round(PM.measured_dt(vs.k, t_draft, t_verify, t_target), 4),
+            "dt_modeled": round(dt_model, 4),
+            "note": "attention only; the paper's dt also counts weights, absent here"}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -524,6 +573,10 @@ def main():
                      "traffic": traffic, "bytes_per_launch": dom_bytes,
                      "avg_launch_ms": round(dom_ms, 5)},
     }
+    if v is not None and d is not None:
+        print("[bench] performance-model times (draft call, verify call, target decode)",
+              file=sys.stderr, flush=True)
+        res["perf_model"] = perf_model_section(v, d, max(3, a.steps // 2))
     if not a.no_cpu_baseline:
         print(f"[bench] cpu baseline (~{a.cpu_seconds}s)", file=sys.stderr, flush=True)
         if is_kvupd:

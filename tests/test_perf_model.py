@@ -1,0 +1,75 @@
+"""Pins of the performance-model calculator (CPU only) against what the paper
+prints and what its formulas imply:
+  * Sec. 6's cost arithmetic: 10 units of decoding save 6.40 (SPIRe, multiplier
+    2.78) and 5.12 (MagicDec, 2.05); net of the 0.25 training cost SPIRe saves
+    6.15, over 20 % more; extrapolated to Llama 3 70B: 6.45 and 5.33, net
+    6.20, over 16 % more;
+  * Sec. 5.2: with k = 4 and N_target = 4 N_draft (the pruned draft keeps two
+    of the eight layers at the same width, so its KV cache is a quarter of the
+    target's too) and every pass memory-bound, L cancels and dt = 2;
+  * Sec. 2's footnote: when drafting and verification are memory-bound, HOI
+    cancels out of dt; in the compute-bound limit dt = (k C_d + (k+1) C_t)/C_t;
+  * the attention-only model on the library's shapes reduces to byte ratios
+    when every pass is memory-bound, and each term is counted by hand."""
+import math
+
+import pytest
+
+from paper_2504_06419_amd import perf_model as PM
+
+
+def test_cost_analysis_numbers():
+    assert round(PM.decode_cost_saved(10, 2.78), 2) == 6.40
+    assert round(PM.decode_cost_saved(10, 2.05), 2) == 5.12
+    assert round(PM.net_saving(10, 2.78, 0.25), 2) == 6.15
+    assert PM.net_saving(10, 2.78, 0.25) / PM.decode_cost_saved(10, 2.05) > 1.20
+    assert round(PM.decode_cost_saved(10, 2.82), 2) == 6.45
+    assert round(PM.decode_cost_saved(10, 2.14), 2) == 5.33
+    assert round(PM.net_saving(10, 2.82, 0.25), 2) == 6.20
+    ratio = PM.net_saving(10, 2.82, 0.25) / PM.decode_cost_saved(10, 2.14)
+    assert 1.16 < ratio < 1.17
+
+
+@pytest.mark.parametrize("kv_t", [1e6, 1e8, 1e10, 1e12])
+@pytest.mark.parametrize("hoi", [50.0, 312.5, 1000.0])
+def test_ablation_dt_is_two_when_memory_bound(kv_t, hoi):
+    n_t = 1.3e8
+    dt = PM.iteration_time_multiplier(k=4, c_draft=1.0, mem_draft=(n_t + kv_t) / 4, c_target=1.0,
+                                      mem_target=n_t + kv_t, hoi_=hoi)
+    assert dt == pytest.approx(2.0, rel=1e-12)
+
+
+def test_hoi_cancels_when_memory_bound_and_compute_limit():
+    a = PM.iteration_time_multiplier(4, 1e3, 3e9, 5e3, 7e9, 100.0)
+    b = PM.iteration_time_multiplier(4, 1e3, 3e9, 5e3, 7e9, 900.0)
+    assert a == pytest.approx(b) == pytest.approx((4 * 3e9 + 7e9) / 7e9)
+    # compute-bound everywhere: HOI small enough that FLOPs dominate
+    c = PM.iteration_time_multiplier(4, 2e12, 1e6, 5e12, 1e6, 1e-3)
+    assert c == pytest.approx((4 * 2e12 + 5 * 5e12) / 5e12)
+
+
+def test_multiplier_and_hoi():
+    assert PM.hoi(2.5e15, 8e12) == pytest.approx(312.5)
+    # the paper's highlighted multipliers with its tau at L = 512 (Table 1)
+    assert PM.throughput_multiplier(3.401, 3.401 / 2.78) == pytest.approx(2.78)
+    assert PM.measured_dt(4, 1.0, 3.0, 2.0) == pytest.approx(3.5)
+
+
+def test_attention_round_counts_and_memory_bound_dt():
+    lens = [100, 5000, 40000]
+    k, Hq, Hkv, D, S, W, es = 8, 64, 8, 128, 4, 4096, 1.0
+    drafts, v, t = PM.attention_round(lens, k, Hq, Hkv, D, S, W, es)
+    g = Hq // Hkv
+    # hand counts: keys per pass, 2 D es bytes and 4 rows D flops per key and KV head
+    keys_t = sum(L + 1 for L in lens)
+    keys_v = sum(L + k + 1 for L in lens)
+    keys_d = [sum(min(L + s + 1, S + W) for L in lens) for s in range(k)]
+    assert t.kv_bytes == 2 * keys_t * Hkv * D * es and t.flops == 4 * g * D * Hkv * keys_t
+    assert v.kv_bytes == 2 * keys_v * Hkv * D * es and v.flops == 4 * (k + 1) * g * D * Hkv * keys_v
+    assert [d.kv_bytes for d in drafts] == [2 * x * Hkv * D * es for x in keys_d]
+    # intensity 2 R / es < HOI: every pass memory-bound, dt is the byte ratio
+    dt = PM.attention_dt(lens, k, Hq, Hkv, D, S, W, es, 625.0)
+    assert dt == pytest.approx((sum(keys_d) + keys_v) / keys_t)
+    # with a tiny HOI the verify pass becomes compute-bound: (k+1) times the target's FLOPs per key
+    dt_c = PM.attention_dt(lens, k, Hq, Hkv, D, S, W, es, 1e-6)
+    assert dt_c == pytest.approx((sum(keys_d) + (k + 1) * keys_v) / keys_t)
