@@ -99,7 +99,11 @@ hipError_t launch_plan(const Problem &p, const Plan &pl, hipStream_t st) {
 }
 
 // One workgroup per segment; segments that one worker covered return at once.
+// The partial slot of every worker covering the segment (or -1 for a worker
+// with an empty range) is worked out once per workgroup into LDS, so the merge
+// loops do no 64-bit divisions.
 __global__ __launch_bounds__(256) void combine_kernel(Problem p, Plan pl) {
+    __shared__ int32_t s_slot[kCombineMaxWorkers];
     const int seg = blockIdx.x;
     const int b = seg / pl.units, u = seg - (seg / pl.units) * pl.units;
     const int tiles = pl.prefix[b + 1] - pl.prefix[b];
@@ -109,33 +113,40 @@ __global__ __launch_bounds__(256) void combine_kernel(Problem p, Plan pl) {
     const int64_t whi = worker_of(start + tiles - 1, T, pl.workers);
     if (wlo == whi) return;
 
+    const int nw = (int)(whi - wlo + 1);  // <= workers <= kCombineMaxWorkers
+    const int64_t begin_lo = worker_begin(wlo, T, pl.workers);
+    for (int i = threadIdx.x; i < nw; i += blockDim.x) {
+        const int64_t w = wlo + i;
+        // workers with an empty range (more workers than tiles) wrote nothing
+        const bool empty = worker_begin(w + 1, T, pl.workers) == worker_begin(w, T, pl.workers);
+        s_slot[i] = empty ? -1 : (int)(2 * w + ((i == 0 && begin_lo < start) ? 1 : 0));
+    }
+    __syncthreads();
+
     // rows of this unit
     const int nrb = pl.units / p.Hkv;  // row blocks per KV head
     const int h = u / nrb;
     const int r0 = (u - h * nrb) * pl.rows;
     const int nrows = p.R - r0 < pl.rows ? p.R - r0 : pl.rows;
     const int d4n = p.D >> 2;
-    const int64_t begin_lo = worker_begin(wlo, T, pl.workers);
 
     for (int idx = threadIdx.x; idx < nrows * d4n; idx += blockDim.x) {
         const int r = idx / d4n, d4 = idx - (idx / d4n) * d4n;
-        // workers with an empty range (more workers than tiles) wrote nothing
         float M = -INFINITY;
-        for (int64_t w = wlo; w <= whi; ++w) {
-            if (worker_begin(w + 1, T, pl.workers) == worker_begin(w, T, pl.workers)) continue;
-            const int64_t slot = 2 * w + ((w == wlo && begin_lo < start) ? 1 : 0);
-            M = fmaxf(M, pl.part_lse[slot * pl.rows + r]);
+        for (int i = 0; i < nw; ++i) {
+            const int slot = s_slot[i];
+            if (slot >= 0) M = fmaxf(M, pl.part_lse[(int64_t)slot * pl.rows + r]);
         }
         float L = 0.f;
         float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
         if (M != -INFINITY) {
-            for (int64_t w = wlo; w <= whi; ++w) {
-                if (worker_begin(w + 1, T, pl.workers) == worker_begin(w, T, pl.workers)) continue;
-                const int64_t slot = 2 * w + ((w == wlo && begin_lo < start) ? 1 : 0);
-                const float lp = pl.part_lse[slot * pl.rows + r];
+            for (int i = 0; i < nw; ++i) {
+                const int slot = s_slot[i];
+                if (slot < 0) continue;
+                const float lp = pl.part_lse[(int64_t)slot * pl.rows + r];
                 const float wgt = lp == -INFINITY ? 0.f : exp2f(lp - M);
                 const float4 o = *reinterpret_cast<const float4 *>(
-                    pl.part_o + (slot * pl.rows + r) * (int64_t)p.D + 4 * d4);
+                    pl.part_o + ((int64_t)slot * pl.rows + r) * (int64_t)p.D + 4 * d4);
                 L += wgt;
                 acc.x += wgt * o.x; acc.y += wgt * o.y; acc.z += wgt * o.z; acc.w += wgt * o.w;
             }
@@ -160,6 +171,7 @@ __global__ __launch_bounds__(256) void combine_kernel(Problem p, Plan pl) {
 hipError_t launch_combine(const Problem &p, const Plan &pl, hipStream_t st) {
     const int64_t segs = (int64_t)p.B * pl.units;
     if (segs == 0) return hipSuccess;
+    if (pl.workers > kCombineMaxWorkers) return hipErrorInvalidValue;
     hipLaunchKernelGGL(combine_kernel, dim3((unsigned)segs), dim3(256), 0, st, p, pl);
     return hipGetLastError();
 }

@@ -226,6 +226,9 @@ spire_status run(Problem &p, bool use_mfma, void *workspace, size_t ws_bytes, hi
     pl.workers = !mf ? generic_workers(cus)
                      : (staged ? staged_workers(cus, nb, p.kv_dtype == SPIRE_FP8_E4M3FN)
                                : mfma_workers(cus));
+    if (pl.workers > kCombineMaxWorkers)
+        return fail(SPIRE_ERR_UNSUPPORTED, "%d workers exceed the combine's limit of %d", pl.workers,
+                    kCombineMaxWorkers);
     const Layout L = layout(p.B, pl.rows, p.D, pl.workers);
     if (ws_bytes < L.total)
         return fail(SPIRE_ERR_WORKSPACE, "workspace has %zu bytes, needs %zu", ws_bytes, L.total);

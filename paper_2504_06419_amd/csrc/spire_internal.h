@@ -29,6 +29,7 @@ namespace spire {
 constexpr int kMaxRows = 128;          // (k+1) * Hq/Hkv
 constexpr int kGenericRowBlock = 16;   // rows per unit in the generic kernel
 constexpr int kMaxWorkersPerCU = 8;
+constexpr int kCombineMaxWorkers = 4096;  // workers one launch may have (the combine's LDS list)
 
 // Device-side description of one K/V view (byte pointers, element strides).
 struct KvDev {
