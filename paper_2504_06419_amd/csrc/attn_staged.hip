@@ -16,8 +16,8 @@
 // every lane reads back its own slots; the V part is row-major (bf16: DMA lane
 // L of instruction t = the 16 bytes of key 4t + L/16 lane L needs; fp8: 8 whole
 // 128-byte rows per instruction, read back 8 bytes per key per lane).  With
-// P = 2, wave 0 copies K and wave 1 copies V; a workgroup barrier per tile
-// publishes both halves.  The compiler does not track the DMA -> LDS
+// P = 2, wave 1 (the one with fewer row blocks) copies whole tiles; a
+// workgroup barrier per tile publishes them.  The compiler does not track the DMA -> LDS
 // dependency, so the kernel waits on vmcnt explicitly before the barrier.
 #include "mfma_common.h"
 
@@ -110,14 +110,16 @@ __device__ __forceinline__ void read_tile(TileRegs<FP8> &T, const lds_u8 *st, in
 }
 
 // One wave's share of a segment: row blocks rb0 .. rb0+NBW-1 over tiles
-// [t0, t1), stage ring shared by the P waves of the workgroup.
-template <bool FP8, int NBW, int MODE, int P, int NS, bool QL>
+// [t0, t1), stage ring shared by the P waves of the workgroup.  COPY says
+// which halves of every tile this wave copies into the ring (1 K, 2 V, 3 both,
+// 0 none).
+template <bool FP8, int NBW, int MODE, int P, int NS, bool QL, int COPY>
 __device__ __forceinline__ void run_segment(const Problem &p, const Plan &pl, lds_u8 *ring,
                                             u32x4 *qlds, const SegAddr &a, int b, int h, int n,
-                                            int t0, int t1, int rb0, int wave, bool whole,
-                                            int64_t slot, int lane) {
+                                            int t0, int t1, int rb0, bool whole, int64_t slot,
+                                            int lane) {
     using G = Stage<FP8>;
-    constexpr int MINE = P == 1 ? G::KLOADS + G::VLOADS : G::KLOADS;  // == VLOADS
+    constexpr int MINE = ((COPY & 1) ? G::KLOADS : 0) + ((COPY & 2) ? G::VLOADS : 0);
     QFrag<NBW, QL> qf;
     if constexpr (QL) qf.lds = qlds;
     SoftmaxState<NBW, true> st;
@@ -129,16 +131,13 @@ __device__ __forceinline__ void run_segment(const Problem &p, const Plan &pl, ld
     if (n > 0) {
         const int last = t1 - 1;
         auto issue = [&](int stage, int tile) {
-            lds_u8 *s = ring + stage * G::BYTES;
-            if (P == 1) issue_tile<FP8, MODE, 3>(s, a, tile, lane);
-            else if (wave == 0) issue_tile<FP8, MODE, 1>(s, a, tile, lane);
-            else issue_tile<FP8, MODE, 2>(s, a, tile, lane);
+            if constexpr (COPY != 0) issue_tile<FP8, MODE, COPY>(ring + stage * G::BYTES, a, tile, lane);
         };
 #pragma unroll
         for (int s = 0; s < NS - 1; ++s) issue(s, t0 + s < last ? t0 + s : last);
         int rd = 0, wr = NS - 1;
         for (int tt = t0; tt <= last; ++tt) {
-            wait_vmcnt<(NS - 2) * MINE>();  // this wave's part of tile tt has landed
+            wait_vmcnt<(NS - 2) * MINE>();  // this wave's copies of tile tt have landed
             ring_barrier();                  // ... and the other waves' parts; tile tt-1 fully read
             issue(wr, tt + NS - 1 < last ? tt + NS - 1 : last);
             wr = wr + 1 == NS ? 0 : wr + 1;
@@ -196,12 +195,17 @@ __global__ __launch_bounds__(64 * P, WPS) void staged_partial_kernel(Problem p, 
         const bool whole = (tile == 0 && t1 == tiles_b);
         const int64_t slot = 2 * (int64_t)wid + (pos == begin ? 0 : 1);
         __syncthreads();  // every wave is done with the ring of the previous segment
-        if (P == 1 || wave == 0)
-            run_segment<FP8, NB0, MODE, P, NS, QL0>(p, pl, ring, qsmem, a, b, h, n, tile, t1, 0,
-                                                    wave, whole, slot, lane);
+        // with two waves, the one with fewer row blocks (wave 1) copies whole
+        // tiles, which evens out the work the two waves do between barriers
+        if (P == 1)
+            run_segment<FP8, NB0, MODE, P, NS, QL0, 3>(p, pl, ring, qsmem, a, b, h, n, tile, t1, 0,
+                                                       whole, slot, lane);
+        else if (wave == 0)
+            run_segment<FP8, NB0, MODE, P, NS, QL0, 0>(p, pl, ring, qsmem, a, b, h, n, tile, t1, 0,
+                                                       whole, slot, lane);
         else
-            run_segment<FP8, NB1, MODE, P, NS, QL1>(p, pl, ring, qsmem + (QL0 ? NB0 : 0) * 4 * 64, a,
-                                                    b, h, n, tile, t1, NB0, wave, whole, slot, lane);
+            run_segment<FP8, NB1, MODE, P, NS, QL1, 3>(p, pl, ring, qsmem + (QL0 ? NB0 : 0) * 4 * 64, a,
+                                                       b, h, n, tile, t1, NB0, whole, slot, lane);
         pos += t1 - tile;
         ++seg;
         tile = 0;
