@@ -84,6 +84,8 @@ def build_workload(name: str, dev):
     t = W.make_token_inputs(wl["token"], seed, device=dev) if "token" in wl else None
     if "kvupd" in wl:
         t = W.make_kvupdate_inputs(wl["kvupd"], seed, device=dev)
+    if "fm" in wl:
+        t = W.make_feedback_inputs(wl["fm"], seed, device=dev)
     return wl, v, d, t
 
 
@@ -195,8 +197,38 @@ def make_kvupd_step(x: W.KvUpdateInputs):
     return step, nbytes, s.B * (s.k + 1), per, (step, view, sink, ring, spk, spv, lens)
 
 
+def make_fm_step(x: W.FeedbackInputs):
+    """One feedback-memory mixing call: reads every layer's activations and
+    the weights once, writes the n_out memory vectors."""
+    s = x.spec
+    out = torch.empty((s.n_out, s.B, s.d), dtype=W.DTYPES[s.m_dtype], device=x.x.device)
+
+    def step():
+        spire.feedback_memory(x.x, x.w, out=out)
+    nbytes = (s.layers * ELEM[s.x_dtype] + s.n_out * ELEM[s.m_dtype]) * s.B * s.d + 4 * x.w.numel()
+    return step, nbytes, s.B, {"feedback_memory": nbytes}
+
+
+def run_cpu_baseline_fm(x: W.FeedbackInputs, budget_s: float):
+    """The feedback-memory oracle (fp64 numpy) on the whole batch, repeated up
+    to the time budget."""
+    from oracle import feedback_memory as FM
+    s = x.spec
+    xs, ws = x.x.float().cpu().numpy(), x.w.cpu().numpy()
+    nbytes = (s.layers * ELEM[s.x_dtype] + s.n_out * ELEM[s.m_dtype]) * s.B * s.d
+    total_t, reps = 0.0, 0
+    while total_t < budget_s and reps < 50:
+        t0 = time.perf_counter()
+        FM.feedback_memory(xs, ws)
+        total_t += time.perf_counter() - t0
+        reps += 1
+    return {"value": reps * nbytes / total_t / 1e9, "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "sample": f"the whole batch, {reps} times", "seconds": round(total_t, 3),
+            "tokens_per_s": reps * s.B / total_t, "tokens_unit": "draft tokens/s"}
+
+
 def dominant_bytes(v, d, dominant, token_step_bytes=None):
-    if dominant in ("token_weights", "draft_append", "kv_append", "draft_rollback"):
+    if dominant in ("token_weights", "draft_append", "kv_append", "draft_rollback", "feedback_memory"):
         return token_step_bytes[dominant] if isinstance(token_step_bytes, dict) else token_step_bytes
     if dominant == "verify_partial":
         return verify_bytes(v)
@@ -364,6 +396,7 @@ KERNEL_SOURCES = ["paper_2504_06419_amd/csrc/attn_mfma.hip",
                   "paper_2504_06419_amd/csrc/attn_staged.hip",
                   "paper_2504_06419_amd/csrc/token_verify.hip",
                   "paper_2504_06419_amd/csrc/kv_update.hip",
+                  "paper_2504_06419_amd/csrc/feedback_memory.hip",
                   "paper_2504_06419_amd/csrc/mfma_common.h",
                   "paper_2504_06419_amd/csrc/spire_internal.h",
                   "paper_2504_06419_amd/build.py"]
@@ -487,7 +520,10 @@ def main():
     wl, v, d, tk = build_workload(a.workload, dev)
     tok_bytes = None
     is_kvupd = isinstance(tk, W.KvUpdateInputs)
-    if is_kvupd:
+    is_fm = isinstance(tk, W.FeedbackInputs)
+    if is_fm:
+        step, nbytes, tokens, tok_bytes = make_fm_step(tk)
+    elif is_kvupd:
         step, nbytes, tokens, tok_bytes, _keep = make_kvupd_step(tk)
     elif tk is not None:
         step, nbytes, tokens, tau = make_token_step(tk)
@@ -527,7 +563,7 @@ def main():
     kavg = {k: sum(x) / len(x) for k, x in per_kernel.items()}
     # the dominant kernel is the attention kernel with the most time per step
     partials = [k for k in ("verify_partial", "draft_partial", "token_weights", "draft_append",
-                            "kv_append", "draft_rollback") if k in per_kernel]
+                            "kv_append", "draft_rollback", "feedback_memory") if k in per_kernel]
     dominant = max(partials, key=lambda k: sum(per_kernel[k]))
     dom_ms = kavg[dominant]
     dom_bytes = dominant_bytes(v, d, dominant, tok_bytes)
@@ -536,7 +572,11 @@ def main():
     traffic = recorded_traffic(a.traffic_json, a.workload, dominant)
 
     gbs = nbytes / (ms * 1e-3) / 1e9
-    if is_kvupd:
+    if is_fm:
+        spec = tk.spec
+        cfg = {"workload": a.workload, "B": spec.B, "d": spec.d, "layers": spec.layers,
+               "n_out": spec.n_out, "x_dtype": spec.x_dtype, "m_dtype": spec.m_dtype}
+    elif is_kvupd:
         spec = tk.spec
         cfg = {"workload": a.workload, "B": spec.B, "Hkv": spec.Hkv, "D": spec.D, "k": spec.k,
                "S": spec.S, "W": spec.W, "kv_dtype": spec.kv_dtype, "new_dtype": "f32",
@@ -558,12 +598,14 @@ def main():
         "metric": METRIC, "value": round(gbs, 2), "unit": "GB/s", "n_gpus": 1, "steps": a.steps,
         "warmup": a.warmup, "ms_per_step": round(ms, 5), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None,
-        "dtype": spec.kv_dtype if is_kvupd else ("f32" if tk is not None else spec.kv_dtype),
+        "dtype": (spec.x_dtype if is_fm else spec.kv_dtype if is_kvupd else
+                  "f32" if tk is not None else spec.kv_dtype),
         "data": "synthetic",
         "config": cfg,
         "frac_of_hbm_peak": round(gbs / HBM_PEAK_GBS, 4),
         "tokens_per_s": round(tokens / (ms * 1e-3), 1),
-        "tokens_unit": ("appended target tokens/s" if is_kvupd else "emitted tokens/s" if tk is not None else
+        "tokens_unit": ("draft tokens/s" if is_fm else "appended target tokens/s" if is_kvupd else
+                        "emitted tokens/s" if tk is not None else
                         "verified tokens/s" if v is not None else "drafted tokens/s"),
         "bytes_per_step": nbytes,
         "kernel_ms": {k: round(x, 5) for k, x in kavg.items()},
@@ -579,7 +621,9 @@ def main():
         res["perf_model"] = perf_model_section(v, d, max(3, a.steps // 2))
     if not a.no_cpu_baseline:
         print(f"[bench] cpu baseline (~{a.cpu_seconds}s)", file=sys.stderr, flush=True)
-        if is_kvupd:
+        if is_fm:
+            res["cpu_baseline"] = run_cpu_baseline_fm(tk, a.cpu_seconds)
+        elif is_kvupd:
             res["cpu_baseline"] = run_cpu_baseline_kvupd(tk, a.cpu_seconds)
         elif tk is not None:
             res["cpu_baseline"] = run_cpu_baseline_token(tk, a.cpu_seconds)

@@ -261,6 +261,24 @@ spire_status spire_draft_rollback(const spire_kv *sink, const spire_kv *ring, co
                                   const int32_t *ring_offset, int32_t B, int32_t Hkv, int32_t D,
                                   int32_t S, int32_t W, hipStream_t stream);
 
+/*
+ * Feedback-memory mixing of the draft (paper Sec. 3.3): the draft is a Feedback
+ * Transformer whose attention reads memory vectors, one per draft layer i,
+ * each a convex mix of the token's activations after every layer (layer 0 is
+ * the embedding):
+ *     m[i] = sum_l exp(w[i][l]) x[l] / sum_l exp(w[i][l]).
+ *   x        [layers, B, d] contiguous, x_dtype SPIRE_F32 or SPIRE_BF16: the
+ *            activations of the step's tokens after each layer.
+ *   w        [n_out, layers] fp32 device array of the learnable weights
+ *            (any finite values; the row maximum is subtracted before exp).
+ *   m        [n_out, B, d] contiguous, m_dtype SPIRE_F32 or SPIRE_BF16 (RNE).
+ *   sizes    1 <= n_out <= 8, 1 <= layers <= 64, B >= 0, d >= 0.
+ * Arithmetic in fp32 (mixing weights and accumulation).  No workspace.
+ */
+spire_status spire_feedback_memory(const void *x, int32_t x_dtype, const float *w, int32_t n_out,
+                                   int32_t layers, int32_t B, int32_t d, void *m, int32_t m_dtype,
+                                   hipStream_t stream);
+
 /* Human-readable name of a status code (static string, never NULL). */
 const char *spire_status_string(spire_status status);
 
@@ -291,7 +309,7 @@ spire_status spire_set_kernel_variant(int32_t variant);
  * returns how many it wrote, then forgets them.  Kernel ids: 0 plan,
  * 1 verify partial attention, 2 draft partial attention, 3 combine,
  * 4 token verification weights, 5 token verification select, 6 kv append,
- * 7 draft append, 8 draft rollback.  At most
+ * 7 draft append, 8 draft rollback, 9 feedback memory.  At most
  * 4096 launches are kept between collects (older ones are dropped).
  * spire_timing_enable(0) releases the events.  Not thread-safe.
  */

@@ -555,6 +555,38 @@ spire_status spire_draft_rollback(const spire_kv *sink, const spire_kv *ring, co
     return SPIRE_OK;
 }
 
+// ---- feedback memory -----------------------------------------------------------
+
+spire_status spire_feedback_memory(const void *x, int32_t x_dtype, const float *w, int32_t n_out,
+                                   int32_t layers, int32_t B, int32_t d, void *m, int32_t m_dtype,
+                                   hipStream_t stream) {
+    g_err[0] = '\0';
+    if (n_out < 1 || n_out > kFmMaxOut)
+        return fail(SPIRE_ERR_UNSUPPORTED, "n_out must be in [1, %d] (got %d)", kFmMaxOut, n_out);
+    if (layers < 1 || layers > kFmMaxLayers)
+        return fail(SPIRE_ERR_UNSUPPORTED, "layers must be in [1, %d] (got %d)", kFmMaxLayers, layers);
+    if (B < 0 || d < 0) return fail(SPIRE_ERR_INVALID_ARG, "need B >= 0 and d >= 0");
+    if ((x_dtype != SPIRE_F32 && x_dtype != SPIRE_BF16) || (m_dtype != SPIRE_F32 && m_dtype != SPIRE_BF16))
+        return fail(SPIRE_ERR_UNSUPPORTED, "x and m must be F32 or BF16");
+    if ((int64_t)B * d == 0) return SPIRE_OK;
+    if (x == nullptr || w == nullptr || m == nullptr) return fail(SPIRE_ERR_INVALID_ARG, "x, w or m is NULL");
+    const uintptr_t xa = x_dtype == SPIRE_F32 ? 3u : 1u, ma = m_dtype == SPIRE_F32 ? 3u : 1u;
+    if (((uintptr_t)x & xa) != 0 || ((uintptr_t)m & ma) != 0 || ((uintptr_t)w & 3u) != 0)
+        return fail(SPIRE_ERR_INVALID_ARG, "arrays must be aligned to their element size");
+    FeedbackArgs a;
+    a.x = x;
+    a.w = w;
+    a.m = m;
+    a.x_dtype = x_dtype;
+    a.m_dtype = m_dtype;
+    a.n_out = n_out;
+    a.Lp1 = layers;
+    a.Bd = (int64_t)B * d;
+    hipError_t e = timed_call(9, stream, [&] { return launch_feedback_memory(a, stream); });
+    if (e != hipSuccess) return fail(SPIRE_ERR_HIP, "feedback memory launch: %s", hipGetErrorString(e));
+    return SPIRE_OK;
+}
+
 spire_status spire_timing_enable(int32_t on) {
     if (on) {
         if (g_timing) return SPIRE_OK;

@@ -174,6 +174,19 @@ hipError_t launch_draft_rollback(const KvDev &sink, const KvDev &ring, const voi
                                  int steps, const int32_t *ring_offset, int B, int Hkv, int D, int S, int W,
                                  hipStream_t st);
 
+// ---- feedback memory (feedback_memory.hip) ------------------------------------
+constexpr int kFmMaxOut = 8;      // memory vectors (draft layers) per call
+constexpr int kFmMaxLayers = 64;  // layers mixed (embedding included)
+struct FeedbackArgs {
+    const void *x;     // [Lp1, B*d]
+    const float *w;    // [n_out, Lp1]
+    void *m;           // [n_out, B*d]
+    int32_t x_dtype, m_dtype;
+    int32_t n_out, Lp1;
+    int64_t Bd;
+};
+hipError_t launch_feedback_memory(const FeedbackArgs &a, hipStream_t st);
+
 // MFMA kernel tile size (keys) and its worker count per CU.
 constexpr int kMfmaTile = 32;
 constexpr int kMfmaWavesPerWG = 4;

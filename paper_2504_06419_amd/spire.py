@@ -25,13 +25,13 @@ STATUS = {0: "SPIRE_OK", 1: "SPIRE_ERR_INVALID_ARG", 2: "SPIRE_ERR_UNSUPPORTED",
 # exported symbols, in the order include/spire.h declares them
 SYMBOLS = ["spire_verify_workspace_size", "spire_verify_attn", "spire_draft_workspace_size",
            "spire_draft_sparse_attn", "spire_token_verify_workspace_size", "spire_token_verify",
-           "spire_kv_append", "spire_draft_append", "spire_draft_rollback",
+           "spire_kv_append", "spire_draft_append", "spire_draft_rollback", "spire_feedback_memory",
            "spire_status_string", "spire_last_error", "spire_version", "spire_set_kernel_variant",
            "spire_timing_enable", "spire_timing_collect"]
 
 KERNEL_IDS = {0: "plan", 1: "verify_partial", 2: "draft_partial", 3: "combine",
               4: "token_weights", 5: "token_select", 6: "kv_append", 7: "draft_append",
-              8: "draft_rollback"}
+              8: "draft_rollback", 9: "feedback_memory"}
 
 
 class SpireError(RuntimeError):
@@ -84,6 +84,8 @@ def load(path: Optional[str] = None):
     L.spire_draft_rollback.restype = C.c_int
     L.spire_draft_rollback.argtypes = [C.POINTER(KV), C.POINTER(KV), vp, vp, vp, vp, i32, vp, i32, i32,
                                        i32, i32, i32, vp]
+    L.spire_feedback_memory.restype = C.c_int
+    L.spire_feedback_memory.argtypes = [vp, i32, vp, i32, i32, i32, i32, vp, i32, vp]
     L.spire_status_string.restype = C.c_char_p
     L.spire_status_string.argtypes = [C.c_int]
     L.spire_last_error.restype = C.c_char_p
@@ -258,6 +260,21 @@ def draft_rollback(sink: KV, ring: KV, spill_k: torch.Tensor, spill_v: torch.Ten
     _check(load().spire_draft_rollback(C.byref(sink), C.byref(ring), spill_k.data_ptr(),
                                        spill_v.data_ptr(), base_lens.data_ptr(), n_accepted.data_ptr(),
                                        steps, ring_offset.data_ptr(), B, Hkv, D, S, W, _stream()))
+
+
+def feedback_memory(x: torch.Tensor, w: torch.Tensor, out: Optional[torch.Tensor] = None,
+                    out_dtype=torch.float32) -> torch.Tensor:
+    """spire_feedback_memory.  x [layers, B, d] (fp32 or bf16), w [n_out, layers] fp32;
+    returns m [n_out, B, d]."""
+    layers, B, d = x.shape
+    n_out = w.shape[0]
+    assert x.is_contiguous() and w.is_contiguous() and w.dtype == torch.float32 and w.shape[1] == layers
+    if out is None:
+        out = torch.empty((n_out, B, d), dtype=out_dtype, device=x.device)
+    assert out.is_contiguous() and out.shape == (n_out, B, d)
+    _check(load().spire_feedback_memory(x.data_ptr(), _DT[x.dtype], w.data_ptr(), n_out, layers, B, d,
+                                        out.data_ptr(), _DT[out.dtype], _stream()))
+    return out
 
 
 def set_kernel_variant(variant: int):

@@ -105,6 +105,19 @@ class KvUpdateSpec:
     accept: float = 0.8     # per-token acceptance of the seeded accepted counts
 
 
+@dataclass
+class FeedbackSpec:
+    """Feedback-memory mixing of one draft step: the activations of the B
+    tokens after each of `layers` layers (embedding included) are mixed into
+    n_out memory vectors, one per draft layer."""
+    B: int
+    d: int
+    layers: int
+    n_out: int
+    x_dtype: str = "bf16"
+    m_dtype: str = "bf16"
+
+
 def named_workloads():
     """The five workloads the library is validated and measured on."""
     return {
@@ -132,6 +145,9 @@ def named_workloads():
         "token_verify_B512_k8_V128256": dict(token=TokenSpec(B=512, k=8, V=128256)),
         "kv_update_round_fp8_B512_k8": dict(kvupd=KvUpdateSpec(B=512, Hkv=8, D=128, k=8, S=4, W=4096,
                                                                 ctx_lo=2048, ctx_hi=65536)),
+        # SPIRe's two-layer draft (embedding + 2 layers mixed into 2 memory
+        # vectors) at the width of Llama 3 70B, the model of Sec. 5.3
+        "feedback_memory_B512_d8192": dict(fm=FeedbackSpec(B=512, d=8192, layers=3, n_out=2)),
     }
 
 
@@ -608,3 +624,21 @@ def make_kvupdate_inputs(spec: KvUpdateSpec, seed: int, device="cpu") -> KvUpdat
                           ring_offset=offs.to(torch.int32).to(device), draft_k=draft_k,
                           draft_v=draft_v, n_accepted=n_acc.to(device), k_scale=dev(k_scale),
                           v_scale=dev(v_scale))
+
+
+# ----------------------------------------------------------------------------
+# Feedback-memory inputs
+# ----------------------------------------------------------------------------
+@dataclass
+class FeedbackInputs:
+    spec: FeedbackSpec
+    x: torch.Tensor   # [layers, B, d]
+    w: torch.Tensor   # fp32 [n_out, layers]
+
+
+def make_feedback_inputs(spec: FeedbackSpec, seed: int, device="cpu") -> FeedbackInputs:
+    """Activations N(0, 1) per layer, weights N(0, 1).  Draw order: weights, activations."""
+    gen = _dev_gen(seed + 49979687, device)
+    w = _randn((spec.n_out, spec.layers), gen, device)
+    x = quantize(_randn((spec.layers, spec.B, spec.d), gen, device), spec.x_dtype)
+    return FeedbackInputs(spec=spec, x=x, w=w)

@@ -271,3 +271,33 @@ def test_draft_rollback_rejects_invalid_arguments(kw, status):
 def test_draft_updates_empty_are_no_ops():
     assert _dappend(B=0, k=None, v=None, lens=None, offs=None) == OK
     assert _rollback(steps=0, sk=None, sv=None, base=None, n=None, offs=None) == OK
+
+
+def _fm(**kw):
+    a = dict(x=FAKE, xdt=spire.BF16, w=FAKE, n=2, layers=3, B=4, d=128, m=FAKE, mdt=spire.BF16)
+    a.update(kw)
+    return spire.load().spire_feedback_memory(a["x"], a["xdt"], a["w"], a["n"], a["layers"], a["B"],
+                                              a["d"], a["m"], a["mdt"], None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(n=0), UNSUPPORTED),
+    (dict(n=9), UNSUPPORTED),
+    (dict(layers=0), UNSUPPORTED),
+    (dict(layers=65), UNSUPPORTED),
+    (dict(B=-1), INVALID),
+    (dict(xdt=spire.FP8), UNSUPPORTED),
+    (dict(mdt=spire.FP8), UNSUPPORTED),
+    (dict(x=None), INVALID),
+    (dict(w=None), INVALID),
+    (dict(m=None), INVALID),
+    (dict(x=FAKE + 1), INVALID),
+    (dict(w=FAKE + 2), INVALID),
+])
+def test_feedback_memory_rejects_invalid_arguments(kw, status):
+    assert _fm(**kw) == status
+
+
+def test_feedback_memory_empty_is_a_no_op():
+    assert _fm(B=0, x=None, w=None, m=None) == OK
+    assert _fm(d=0, x=None, w=None, m=None) == OK
