@@ -111,9 +111,17 @@ __global__ __launch_bounds__(64) void generic_partial_kernel(Problem p, Plan pl)
         const int u = seg - b * pl.units;
         const int h = u / nrb;
         const int r0 = (u - h * nrb) * RB;
-        const int tiles_b = pl.prefix[b + 1] - pl.prefix[b];
+        const int span = pl.prefix[b + 1] - pl.prefix[b];
+        const int tiles_b = span - pl.seg_cost;
         const int64_t left = end - pos;
-        const int t1 = left < (int64_t)(tiles_b - tile) ? tile + (int)left : tiles_b;
+        const int te = left < (int64_t)(span - tile) ? tile + (int)left : span;
+        if (tile >= tiles_b) {  // phantom positions only
+            pos += te - tile;
+            ++seg;
+            tile = 0;
+            continue;
+        }
+        const int t1 = te < tiles_b ? te : tiles_b;
         const int n = pl.nkeys[b];
         int ns = 0, rs = 0;
         if (p.draft) {
@@ -224,7 +232,7 @@ __global__ __launch_bounds__(64) void generic_partial_kernel(Problem p, Plan pl)
                 if (lane == 0) pl.part_lse[slot * pl.rows + r] = lse2;
             }
         }
-        pos += t1 - tile;
+        pos += te - tile;
         ++seg;
         tile = 0;
     }

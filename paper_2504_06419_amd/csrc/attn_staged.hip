@@ -187,9 +187,17 @@ __global__ __launch_bounds__(64 * P, WPS) void staged_partial_kernel(Problem p, 
     while (pos < end) {
         const int b = seg / pl.units;
         const int h = seg - b * pl.units;
-        const int tiles_b = uload(pl.prefix, b + 1) - uload(pl.prefix, b);
+        const int span = uload(pl.prefix, b + 1) - uload(pl.prefix, b);
+        const int tiles_b = span - pl.seg_cost;
         const int64_t left = end - pos;
-        const int t1 = left < (int64_t)(tiles_b - tile) ? tile + (int)left : tiles_b;
+        const int te = left < (int64_t)(span - tile) ? tile + (int)left : span;
+        if (tile >= tiles_b) {  // phantom positions only
+            pos += te - tile;
+            ++seg;
+            tile = 0;
+            continue;
+        }
+        const int t1 = te < tiles_b ? te : tiles_b;
         const int n = uload(pl.nkeys, b);
         const SegAddr a = make_seg_addr<MODE>(p, b, h, n);
         const bool whole = (tile == 0 && t1 == tiles_b);
@@ -206,7 +214,7 @@ __global__ __launch_bounds__(64 * P, WPS) void staged_partial_kernel(Problem p, 
         else
             run_segment<FP8, NB1, MODE, P, NS, QL1, 3>(p, pl, ring, qsmem + (QL0 ? NB0 : 0) * 4 * 64, a,
                                                        b, h, n, tile, t1, NB0, whole, slot, lane);
-        pos += t1 - tile;
+        pos += te - tile;
         ++seg;
         tile = 0;
     }

@@ -48,8 +48,8 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(Problem p, Plan pl) 
     for (int b = b0; b < b1; ++b) {
         const int n = effective_keys(p, b);
         pl.nkeys[b] = n;
-        const int tiles = n > 0 ? (n + pl.tile - 1) / pl.tile : 1;
-        prefix[b] = tiles;  // temporarily the tile count
+        const int tiles = (n > 0 ? (n + pl.tile - 1) / pl.tile : 1) + pl.seg_cost;
+        prefix[b] = tiles;  // temporarily the position count
         local += tiles;
     }
     sums[tid] = local;
@@ -106,9 +106,11 @@ __global__ __launch_bounds__(256) void combine_kernel(Problem p, Plan pl) {
     __shared__ int32_t s_slot[kCombineMaxWorkers];
     const int seg = blockIdx.x;
     const int b = seg / pl.units, u = seg - (seg / pl.units) * pl.units;
-    const int tiles = pl.prefix[b + 1] - pl.prefix[b];
+    const int span = pl.prefix[b + 1] - pl.prefix[b];  // tiles + phantom positions
+    const int tiles = span - pl.seg_cost;
     const int64_t T = (int64_t)pl.prefix[p.B] * pl.units;
-    const int64_t start = (int64_t)pl.prefix[b] * pl.units + (int64_t)u * tiles;
+    const int64_t start = (int64_t)pl.prefix[b] * pl.units + (int64_t)u * span;
+    // the workers whose ranges hold the segment's tiles (phantoms are not read)
     const int64_t wlo = worker_of(start, T, pl.workers);
     const int64_t whi = worker_of(start + tiles - 1, T, pl.workers);
     if (wlo == whi) return;

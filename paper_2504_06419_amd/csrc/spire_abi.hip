@@ -226,6 +226,13 @@ spire_status run(Problem &p, bool use_mfma, void *workspace, size_t ws_bytes, hi
     pl.workers = !mf ? generic_workers(cus)
                      : (staged ? staged_workers(cus, nb, p.kv_dtype == SPIRE_FP8_E4M3FN)
                                : mfma_workers(cus));
+    // phantom positions per segment (spire_internal.h): on the matrix-core
+    // kernels a worker's time grew by about as much per segment it covered as
+    // streaming 35-40 KB of keys takes (queries, output rows, address set-up,
+    // pipeline refill); without this, workers covering many short sequences
+    // finished last
+    const int64_t tile_bytes = 2LL * kMfmaTile * p.D * p.kv.elem;
+    pl.seg_cost = mf ? (int)((40960 + tile_bytes / 2) / tile_bytes) : 0;
     if (pl.workers > kCombineMaxWorkers)
         return fail(SPIRE_ERR_UNSUPPORTED, "%d workers exceed the combine's limit of %d", pl.workers,
                     kCombineMaxWorkers);

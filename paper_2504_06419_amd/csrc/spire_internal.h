@@ -5,10 +5,14 @@
 //     with no key still owns one (empty) tile so that its rows get written;
 //   * a segment is one (sequence b, unit u) pair, where a unit is one KV head
 //     (matrix-core kernels) or one KV head x 16-row block (generic kernel);
-//     segment s = b * units + u owns tiles_b consecutive positions;
-//   * the flattened positions [0, T), T = units * sum_b tiles_b, are split into
-//     `workers` contiguous ranges of equal length: worker w owns
-//     [w*T/workers, (w+1)*T/workers);
+//     segment s = b * units + u owns tiles_b + seg_cost consecutive positions:
+//     its tiles followed by seg_cost phantom positions that stand for the
+//     fixed cost of a segment (queries, output rows, address set-up), so that
+//     a worker covering many short segments gets correspondingly fewer tiles;
+//     a worker reads no keys for phantom positions;
+//   * the flattened positions [0, T), T = units * sum_b (tiles_b + seg_cost),
+//     are split into `workers` contiguous ranges of equal length: worker w
+//     owns [w*T/workers, (w+1)*T/workers);
 //   * a worker that covers a whole segment writes the final rows; otherwise it
 //     writes a partial (normalised output + base-2 log-sum-exp) into slot 2w
 //     (the segment it starts in) or 2w+1 (the segment it ends in), and the
@@ -70,7 +74,7 @@ struct Problem {
 // Partition state in the workspace.
 struct Plan {
     int32_t *nkeys;     // [B]   keys of each sequence after clamping
-    int32_t *prefix;    // [B+1] exclusive prefix sum of tiles per sequence
+    int32_t *prefix;    // [B+1] exclusive prefix sum of tiles + seg_cost per sequence
     int32_t *wstart;    // [2*workers] (segment, tile) where each worker starts
     float *part_lse;    // [2*workers, rows]       base-2 log-sum-exp of a partial
     float *part_o;      // [2*workers, rows, D]    normalised partial output
@@ -78,6 +82,7 @@ struct Plan {
     int32_t units;      // segments per sequence
     int32_t rows;       // rows per segment (partials stride)
     int32_t workers;
+    int32_t seg_cost;   // phantom positions per segment (see above)
 };
 
 // Read-only, wave-uniform metadata (block tables, prefix sums, lengths,

@@ -301,7 +301,8 @@ def test_round_fp8_B512_k8():
 
 def test_plan_partition_invariants():
     """The plan kernel's output read back from the workspace (layout of
-    spire_abi.hip): clamped key counts, tile prefix sums, worker start points."""
+    spire_abi.hip): clamped key counts, prefix sums of tile + phantom positions,
+    worker start points."""
     banner("plan partition")
     spec = W.VerifySpec(B=37, Hq=32, Hkv=8, D=128, k=4, ctx_lo=1, ctx_hi=5000, page_size=16)
     inp = W.make_verify_inputs(spec, 14, device=DEV)
@@ -323,7 +324,10 @@ def test_plan_partition_invariants():
     workers = torch.cuda.get_device_properties(0).multi_processor_count * 4
     wstart = raw[o2:o2 + 8 * workers].view(torch.int32).view(-1, 2)
     assert nkeys.tolist() == torch.clamp(lens.cpu(), 0, cap).tolist()
-    tiles = [max(1, (n + tile - 1) // tile) for n in nkeys.tolist()]
+    # every segment also owns phantom positions for its fixed cost: the
+    # equivalent of 40 KB of tiles, 3 tiles of 32 bf16 keys x 128 dims x (K, V)
+    seg_cost = 3
+    tiles = [max(1, (n + tile - 1) // tile) + seg_cost for n in nkeys.tolist()]
     assert prefix.tolist() == [sum(tiles[:b]) for b in range(B + 1)]
     T = prefix[B].item() * units
     covered = 0
