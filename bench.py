@@ -14,6 +14,9 @@ Prints ONE JSON line: value = algorithmic HBM bytes per step / time per step
 (GB/s), plus verified tokens/s, the roofline of the dominant kernel (its
 average duration from HIP events recorded around each of its launches on the
 launch stream) and the CPU oracle timed on a bounded sample of the same batch.
+Also: per-step times with cold caches (a 512 MiB scratch write before each of
+20 steps; median, 10th and 90th percentile) and the HBM read rate of a plain
+streaming-read kernel over 4 GiB, the practical ceiling next to 8 TB/s.
 """
 from __future__ import annotations
 
@@ -487,6 +490,52 @@ def perf_model_section(v: W.VerifyInputs, d: W.DraftInputs, reps: int) -> dict:
             "note": "attention only; the paper's dt also counts weights, absent here"}
 
 
+def flushed_step_times(step, iters: int = 20, flush_bytes: int = 512 << 20) -> dict:
+    """Per-step times with cold caches: before every step a 512 MiB scratch
+    write evicts the L2s and the 256 MB Infinity Cache, then one step runs
+    between two events on the launch stream.  Median and 10th/90th
+    percentiles in ms."""
+    st = torch.cuda.current_stream()
+    scratch = torch.empty((flush_bytes,), dtype=torch.uint8, device="cuda")
+    times = []
+    for i in range(iters):
+        scratch.fill_(i & 0xFF)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(st)
+        step()
+        e1.record(st)
+        torch.cuda.synchronize()
+        times.append(e0.elapsed_time(e1))
+    del scratch
+    q = lambda f: float(np.percentile(times, f))
+    return {"iters": iters, "flush_bytes": flush_bytes, "median_ms": round(q(50), 5),
+            "p10_ms": round(q(10), 5), "p90_ms": round(q(90), 5)}
+
+
+def read_ceiling(nbytes: int = 4 << 30, reps: int = 10) -> dict:
+    """HBM read rate of the library's plain streaming-read probe over a 4 GiB
+    buffer (HIP events around each launch): the practical ceiling beside the
+    8 TB/s specification."""
+    buf = torch.empty((nbytes,), dtype=torch.uint8, device="cuda")
+    buf.fill_(1)
+    sink = torch.empty((spire.HBM_PROBE_SINK_WORDS,), dtype=torch.int32, device="cuda")
+    for _ in range(2):
+        spire.hbm_read_probe(buf, sink)
+    torch.cuda.synchronize()
+    spire.timing_enable(True)
+    spire.timing_collect()
+    for _ in range(reps):
+        spire.hbm_read_probe(buf, sink)
+    torch.cuda.synchronize()
+    ms = [t for name, t in spire.timing_collect() if name == "hbm_read_probe"]
+    spire.timing_enable(False)
+    del buf
+    avg = sum(ms) / len(ms)
+    gbs = nbytes / (avg * 1e-3) / 1e9
+    return {"gbs": round(gbs, 1), "frac_of_spec": round(gbs / HBM_PEAK_GBS, 4), "bytes": nbytes,
+            "reps": reps, "avg_launch_ms": round(avg, 5)}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -571,6 +620,11 @@ def main():
 
     traffic = recorded_traffic(a.traffic_json, a.workload, dominant)
 
+    print("[bench] flushed per-step times", file=sys.stderr, flush=True)
+    flushed = flushed_step_times(step)
+    print("[bench] streaming-read ceiling", file=sys.stderr, flush=True)
+    ceiling = read_ceiling()
+
     gbs = nbytes / (ms * 1e-3) / 1e9
     if is_fm:
         spec = tk.spec
@@ -614,6 +668,9 @@ def main():
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": traffic, "bytes_per_launch": dom_bytes,
                      "avg_launch_ms": round(dom_ms, 5)},
+        "step_ms_flushed": flushed,
+        "read_ceiling": dict(ceiling, frac_step=round(gbs / ceiling["gbs"], 4),
+                             frac_dominant=round(achieved / ceiling["gbs"], 4)),
     }
     if v is not None and d is not None:
         print("[bench] performance-model times (draft call, verify call, target decode)",

@@ -279,6 +279,24 @@ spire_status spire_feedback_memory(const void *x, int32_t x_dtype, const float *
                                    int32_t layers, int32_t B, int32_t d, void *m, int32_t m_dtype,
                                    hipStream_t stream);
 
+/*
+ * Streaming-read probe (a measurement aid, not a step of the method): reads
+ * the `bytes` bytes at device pointer `buf` once with 16-byte nontemporal
+ * loads, as a plain streaming kernel does, and writes an XOR fold of what it
+ * read to the device array `sink`, which must hold
+ * SPIRE_HBM_PROBE_SINK_WORDS words (every word is written; the XOR of all of
+ * them equals the XOR of every 32-bit word of the buffer).  Its duration gives
+ * the HBM read rate this device reaches in practice, the ceiling the
+ * attention kernels are compared against beside the 8 TB/s specification.
+ *   buf   16-byte aligned, bytes a multiple of 16 (0 is allowed: nothing read,
+ *         the sink still written);
+ *   sink  4-byte aligned.
+ * Asynchronous on `stream`; allocates nothing.  Kernel id 10 in the timing
+ * records.
+ */
+#define SPIRE_HBM_PROBE_SINK_WORDS 2048
+spire_status spire_hbm_read_probe(const void *buf, size_t bytes, uint32_t *sink, hipStream_t stream);
+
 /* Human-readable name of a status code (static string, never NULL). */
 const char *spire_status_string(spire_status status);
 
@@ -309,7 +327,8 @@ spire_status spire_set_kernel_variant(int32_t variant);
  * returns how many it wrote, then forgets them.  Kernel ids: 0 plan,
  * 1 verify partial attention, 2 draft partial attention, 3 combine,
  * 4 token verification weights, 5 token verification select, 6 kv append,
- * 7 draft append, 8 draft rollback, 9 feedback memory.  At most
+ * 7 draft append, 8 draft rollback, 9 feedback memory, 10 streaming-read
+ * probe.  At most
  * 4096 launches are kept between collects (older ones are dropped).
  * spire_timing_enable(0) releases the events.  Not thread-safe.
  */

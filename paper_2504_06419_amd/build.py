@@ -19,7 +19,7 @@ ARCH = "gfx950"
 
 SOURCES = ["spire_abi.hip", "plan_combine.hip", "attn_mfma.hip", "attn_staged.hip",
            "attn_generic.hip", "token_verify.hip", "kv_update.hip",
-           "feedback_memory.hip"]
+           "feedback_memory.hip", "hbm_probe.hip"]
 
 FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

@@ -594,6 +594,18 @@ spire_status spire_feedback_memory(const void *x, int32_t x_dtype, const float *
     return SPIRE_OK;
 }
 
+spire_status spire_hbm_read_probe(const void *buf, size_t bytes, uint32_t *sink, hipStream_t stream) {
+    g_err[0] = '\0';
+    if (sink == nullptr || (bytes > 0 && buf == nullptr)) return fail(SPIRE_ERR_INVALID_ARG, "buf or sink is NULL");
+    if (((uintptr_t)buf & 15u) != 0 || bytes % 16 != 0)
+        return fail(SPIRE_ERR_INVALID_ARG, "buf must be 16-byte aligned and bytes a multiple of 16");
+    if (((uintptr_t)sink & 3u) != 0) return fail(SPIRE_ERR_INVALID_ARG, "sink must be 4-byte aligned");
+    if (bytes > (size_t)INT64_MAX) return fail(SPIRE_ERR_INVALID_ARG, "bytes too large");
+    hipError_t e = timed_call(10, stream, [&] { return launch_hbm_read(buf, (int64_t)bytes, sink, stream); });
+    if (e != hipSuccess) return fail(SPIRE_ERR_HIP, "read probe launch: %s", hipGetErrorString(e));
+    return SPIRE_OK;
+}
+
 spire_status spire_timing_enable(int32_t on) {
     if (on) {
         if (g_timing) return SPIRE_OK;

@@ -146,6 +146,7 @@ constexpr int staged_waves(int nb) { return nb <= 2 ? 1 : 2; }
 constexpr int staged_wps(bool fp8, int nb) { return fp8 && nb > 2 ? 2 : 1; }
 int staged_workers(int cus, int nb, bool fp8);
 hipError_t launch_combine(const Problem &p, const Plan &pl, hipStream_t st);
+hipError_t launch_hbm_read(const void *buf, int64_t bytes, uint32_t *sink, hipStream_t st);
 
 // ---- token verification (token_verify.hip) -----------------------------------
 constexpr int kTokenPiece = 2048;    // vocabulary entries per weights wave

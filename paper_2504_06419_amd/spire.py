@@ -27,11 +27,12 @@ SYMBOLS = ["spire_verify_workspace_size", "spire_verify_attn", "spire_draft_work
            "spire_draft_sparse_attn", "spire_token_verify_workspace_size", "spire_token_verify",
            "spire_kv_append", "spire_draft_append", "spire_draft_rollback", "spire_feedback_memory",
            "spire_status_string", "spire_last_error", "spire_version", "spire_set_kernel_variant",
-           "spire_timing_enable", "spire_timing_collect"]
+           "spire_timing_enable", "spire_timing_collect", "spire_hbm_read_probe"]
 
 KERNEL_IDS = {0: "plan", 1: "verify_partial", 2: "draft_partial", 3: "combine",
               4: "token_weights", 5: "token_select", 6: "kv_append", 7: "draft_append",
-              8: "draft_rollback", 9: "feedback_memory"}
+              8: "draft_rollback", 9: "feedback_memory", 10: "hbm_read_probe"}
+HBM_PROBE_SINK_WORDS = 2048
 
 
 class SpireError(RuntimeError):
@@ -93,6 +94,8 @@ def load(path: Optional[str] = None):
     L.spire_version.restype = i32
     L.spire_set_kernel_variant.restype = C.c_int
     L.spire_set_kernel_variant.argtypes = [i32]
+    L.spire_hbm_read_probe.restype = C.c_int
+    L.spire_hbm_read_probe.argtypes = [vp, sz, vp, vp]
     L.spire_timing_enable.restype = C.c_int
     L.spire_timing_enable.argtypes = [i32]
     L.spire_timing_collect.restype = i32
@@ -279,6 +282,18 @@ def feedback_memory(x: torch.Tensor, w: torch.Tensor, out: Optional[torch.Tensor
 
 def set_kernel_variant(variant: int):
     _check(load().spire_set_kernel_variant(variant))
+
+
+def hbm_read_probe(buf: torch.Tensor, sink: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """spire_hbm_read_probe: stream `buf` (contiguous, 16-byte aligned, a
+    multiple of 16 bytes) once; returns the int32 sink of XOR folds."""
+    assert buf.is_contiguous() and buf.is_cuda
+    if sink is None:
+        sink = torch.empty((HBM_PROBE_SINK_WORDS,), dtype=torch.int32, device=buf.device)
+    assert sink.dtype == torch.int32 and sink.numel() >= HBM_PROBE_SINK_WORDS
+    _check(load().spire_hbm_read_probe(buf.data_ptr(), buf.numel() * buf.element_size(),
+                                       sink.data_ptr(), _stream()))
+    return sink
 
 
 def timing_enable(on: bool):

@@ -119,7 +119,7 @@ class FeedbackSpec:
 
 
 def named_workloads():
-    """The five workloads the library is validated and measured on."""
+    """The workloads the library is validated and measured on."""
     return {
         "tiny_f32": dict(
             verify=VerifySpec(B=4, Hq=8, Hkv=2, D=64, k=4, ctx_lo=512, ctx_hi=512,
@@ -148,6 +148,11 @@ def named_workloads():
         # SPIRe's two-layer draft (embedding + 2 layers mixed into 2 memory
         # vectors) at the width of Llama 3 70B, the model of Sec. 5.3
         "feedback_memory_B512_d8192": dict(fm=FeedbackSpec(B=512, d=8192, layers=3, n_out=2)),
+        # one GPU's share of the fp8 round's verification under tensor
+        # parallelism over the 8 KV heads: 8 query heads reading 1 KV head
+        "verify_tp8shard_fp8_B512_k8": dict(
+            verify=VerifySpec(B=512, Hq=8, Hkv=1, D=128, k=8, ctx_lo=2048, ctx_hi=65536,
+                              kv_dtype="fp8", page_size=16, spare_pages=64)),
     }
 
 

@@ -301,3 +301,18 @@ def test_feedback_memory_rejects_invalid_arguments(kw, status):
 def test_feedback_memory_empty_is_a_no_op():
     assert _fm(B=0, x=None, w=None, m=None) == OK
     assert _fm(d=0, x=None, w=None, m=None) == OK
+
+
+def _probe(buf=FAKE, nbytes=1 << 20, sink=FAKE):
+    return spire.load().spire_hbm_read_probe(buf, nbytes, sink, None)
+
+
+@pytest.mark.parametrize("kw", [
+    dict(sink=None),
+    dict(buf=None),
+    dict(buf=FAKE + 8),
+    dict(nbytes=(1 << 20) + 4),
+    dict(sink=FAKE + 2),
+])
+def test_hbm_read_probe_rejects_invalid_arguments(kw):
+    assert _probe(**kw) == INVALID

@@ -299,6 +299,14 @@ def test_round_fp8_B512_k8():
     _check_verify(inp, TOL["fp8"], seq_ids=ids)
 
 
+def test_verify_tp8shard_fp8_B512_k8():
+    banner("verify_tp8shard_fp8_B512_k8: one tensor-parallel shard of the fp8 verify")
+    name = "verify_tp8shard_fp8_B512_k8"
+    inp = W.make_verify_inputs(NW[name]["verify"], W.MASTER_SEED + W.WORKLOAD_INDEX[name], device=DEV)
+    ids = sample_ids(inp.kv_lens.tolist(), 6, seed=9)
+    _check_verify(inp, TOL["fp8"], seq_ids=ids)
+
+
 def test_plan_partition_invariants():
     """The plan kernel's output read back from the workspace (layout of
     spire_abi.hip): clamped key counts, prefix sums of tile + phantom positions,
