@@ -98,10 +98,11 @@ hipError_t launch_plan(const Problem &p, const Plan &pl, hipStream_t st) {
     return hipGetLastError();
 }
 
-// One workgroup per segment; segments that one worker covered return at once.
-// The partial slot of every worker covering the segment (or -1 for a worker
-// with an empty range) is worked out once per workgroup into LDS, so the merge
-// loops do no 64-bit divisions.
+// Workgroup (segment, row chunk): a segment's rows are split into gridDim.y
+// chunks, one thread per 4 output elements; workgroups of segments that one
+// worker covered return at once.  The partial slot of every worker covering the segment (or -1 for a
+// worker with an empty range) is worked out once per workgroup into LDS, so
+// the merge loops do no 64-bit divisions.
 __global__ __launch_bounds__(256) void combine_kernel(Problem p, Plan pl) {
     __shared__ int32_t s_slot[kCombineMaxWorkers];
     const int seg = blockIdx.x;
@@ -125,15 +126,17 @@ __global__ __launch_bounds__(256) void combine_kernel(Problem p, Plan pl) {
     }
     __syncthreads();
 
-    // rows of this unit
+    // rows of this unit, and the element of this thread
     const int nrb = pl.units / p.Hkv;  // row blocks per KV head
     const int h = u / nrb;
     const int r0 = (u - h * nrb) * pl.rows;
     const int nrows = p.R - r0 < pl.rows ? p.R - r0 : pl.rows;
     const int d4n = p.D >> 2;
-
-    for (int idx = threadIdx.x; idx < nrows * d4n; idx += blockDim.x) {
-        const int r = idx / d4n, d4 = idx - (idx / d4n) * d4n;
+    const int rpc = (pl.rows + gridDim.y - 1) / gridDim.y;  // rows per chunk
+    const int rlo = blockIdx.y * rpc;
+    const int rhi = rlo + rpc < nrows ? rlo + rpc : nrows;
+    for (int idx = threadIdx.x; idx < (rhi - rlo) * d4n; idx += blockDim.x) {
+        const int r = rlo + idx / d4n, d4 = idx - (idx / d4n) * d4n;
         float M = -INFINITY;
         for (int i = 0; i < nw; ++i) {
             const int slot = s_slot[i];
@@ -174,7 +177,15 @@ hipError_t launch_combine(const Problem &p, const Plan &pl, hipStream_t st) {
     const int64_t segs = (int64_t)p.B * pl.units;
     if (segs == 0) return hipSuccess;
     if (pl.workers > kCombineMaxWorkers) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(combine_kernel, dim3((unsigned)segs), dim3(256), 0, st, p, pl);
+    // split the rows of a segment over up to one workgroup per 256 outputs
+    // while there are few segments (at most ~4096 workgroups in all: most of
+    // them belong to segments that need no merge and return at once, and more
+    // measured slower at 4096 segments)
+    const int rpw = 256 / (p.D / 4);
+    const int64_t want = (pl.rows + rpw - 1) / rpw;
+    const int64_t room = segs >= 4096 ? 1 : 4096 / segs;
+    const unsigned chunks = (unsigned)(want < room ? want : room);
+    hipLaunchKernelGGL(combine_kernel, dim3((unsigned)segs, chunks), dim3(256), 0, st, p, pl);
     return hipGetLastError();
 }
 
