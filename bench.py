@@ -397,6 +397,8 @@ def run_cpu_baseline(v, d, budget_s: float):
 # ---------------------------------------------------------------------------
 KERNEL_SOURCES = ["paper_2504_06419_amd/csrc/attn_mfma.hip",
                   "paper_2504_06419_amd/csrc/attn_staged.hip",
+                  "paper_2504_06419_amd/csrc/plan_combine.hip",
+                  "paper_2504_06419_amd/csrc/spire_abi.hip",
                   "paper_2504_06419_amd/csrc/token_verify.hip",
                   "paper_2504_06419_amd/csrc/kv_update.hip",
                   "paper_2504_06419_amd/csrc/feedback_memory.hip",
@@ -544,6 +546,8 @@ def main():
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD, choices=list(W.named_workloads()))
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="skip the cold-cache step times and the read-ceiling probe (profiler runs)")
     ap.add_argument("--traffic-json", default=os.path.join(ROOT, "profiles", "hbm_traffic.json"))
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a 4 GiB device copy (counter calibration) and exit")
@@ -620,10 +624,12 @@ def main():
 
     traffic = recorded_traffic(a.traffic_json, a.workload, dominant)
 
-    print("[bench] flushed per-step times", file=sys.stderr, flush=True)
-    flushed = flushed_step_times(step)
-    print("[bench] streaming-read ceiling", file=sys.stderr, flush=True)
-    ceiling = read_ceiling()
+    flushed = ceiling = None
+    if not a.no_extras:
+        print("[bench] flushed per-step times", file=sys.stderr, flush=True)
+        flushed = flushed_step_times(step)
+        print("[bench] streaming-read ceiling", file=sys.stderr, flush=True)
+        ceiling = read_ceiling()
 
     gbs = nbytes / (ms * 1e-3) / 1e9
     if is_fm:
@@ -668,10 +674,11 @@ def main():
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": traffic, "bytes_per_launch": dom_bytes,
                      "avg_launch_ms": round(dom_ms, 5)},
-        "step_ms_flushed": flushed,
-        "read_ceiling": dict(ceiling, frac_step=round(gbs / ceiling["gbs"], 4),
-                             frac_dominant=round(achieved / ceiling["gbs"], 4)),
     }
+    if ceiling is not None:
+        res["step_ms_flushed"] = flushed
+        res["read_ceiling"] = dict(ceiling, frac_step=round(gbs / ceiling["gbs"], 4),
+                                   frac_dominant=round(achieved / ceiling["gbs"], 4))
     if v is not None and d is not None:
         print("[bench] performance-model times (draft call, verify call, target decode)",
               file=sys.stderr, flush=True)
