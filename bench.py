@@ -212,6 +212,17 @@ def make_fm_step(x: W.FeedbackInputs):
     return step, nbytes, s.B, {"feedback_memory": nbytes}
 
 
+def cpu_model() -> str:
+    """The host CPU's model name (recorded beside the CPU baseline)."""
+    try:
+        for ln in open("/proc/cpuinfo"):
+            if ln.startswith("model name"):
+                return ln.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def run_cpu_baseline_fm(x: W.FeedbackInputs, budget_s: float):
     """The feedback-memory oracle (fp64 numpy) on the whole batch, repeated up
     to the time budget."""
@@ -693,6 +704,7 @@ def main():
             res["cpu_baseline"] = run_cpu_baseline_token(tk, a.cpu_seconds)
         else:
             res["cpu_baseline"] = run_cpu_baseline(v, d, a.cpu_seconds)
+        res["cpu_baseline"]["cpu_model"] = cpu_model()
     print(json.dumps(res), flush=True)
 
 
