@@ -66,13 +66,37 @@ def _paged_cache(gen, dtype, B, Hkv, D, ps, lens, T, spare=3):
     return k.to(DEV), v.to(DEV), table
 
 
+def _on_device(x, offset):
+    """x on the GPU, `offset` elements past an aligned allocation (offset 1
+    misaligns the rows for the 4-element vector path)."""
+    if offset == 0:
+        return x.to(DEV).contiguous()
+    buf = torch.empty((x.numel() + offset,), dtype=x.dtype, device=DEV)
+    out = buf[offset:].view(x.shape)
+    out.copy_(x.to(DEV))
+    return out
+
+
 @pytest.mark.parametrize("dtype", ["f32", "bf16", "fp8"])
 @pytest.mark.parametrize("src", ["f32", "bf16"])
 @pytest.mark.parametrize("paged", [True, False])
 def test_kv_append_matches_oracle(dtype, src, paged):
-    banner(f"kv append storage={dtype} input={src} paged={paged}")
-    gen = torch.Generator().manual_seed(300 + 7 * len(dtype) + len(src) + int(paged))
-    B, Hkv, D, T, ps = 6, 2, 128, 5, 16
+    _kv_append_case(dtype, src, paged)
+
+
+# the element-by-element path: head dims that are not a multiple of 4, and
+# inputs that do not start on a 4-element boundary
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "fp8"])
+@pytest.mark.parametrize("paged", [True, False])
+@pytest.mark.parametrize("D,offset", [(30, 0), (128, 1)])
+def test_kv_append_scalar_path_matches_oracle(dtype, paged, D, offset):
+    _kv_append_case(dtype, "f32", paged, D=D, offset=offset)
+
+
+def _kv_append_case(dtype, src, paged, D=128, offset=0):
+    banner(f"kv append storage={dtype} input={src} paged={paged} D={D} input offset={offset}")
+    gen = torch.Generator().manual_seed(300 + 7 * len(dtype) + len(src) + int(paged) + D + offset)
+    B, Hkv, T, ps = 6, 2, 5, 16
     lens = torch.randint(0, 40, (B,), generator=gen)
     lens[1] = -3          # negative start: the first positions are skipped
     kn = special_values(gen, (B, T, Hkv, D))
@@ -102,7 +126,7 @@ def test_kv_append_matches_oracle(dtype, src, paged):
         table = None
         view = spire.kv_view(kc, vc, k_scale=ks_d, v_scale=vs_d)
     hk, hv = host_bytes(kc, dtype), host_bytes(vc, dtype)
-    spire.kv_append(view, kn.to(DEV).contiguous(), vn.to(DEV).contiguous(), lens.to(torch.int32).to(DEV))
+    spire.kv_append(view, _on_device(kn, offset), _on_device(vn, offset), lens.to(torch.int32).to(DEV))
     torch.cuda.synchronize()
     KU.kv_append(hk, hv, kn.float().numpy(), vn.float().numpy(), lens.numpy(), dtype,
                  ps if paged else 0, None if table is None else table.numpy(),
@@ -129,9 +153,21 @@ def _draft_cache(gen, dtype, B, Hkv, D, S, Wn):
 @pytest.mark.parametrize("S,Wn,lo,hi", [(4, 64, 100, 200), (4, 64, 1, 40), (0, 16, 1, 30),
                                         (2, 2, 1, 20), (3, 0, 1, 6)])
 def test_draft_append_and_rollback_match_oracle(dtype, S, Wn, lo, hi):
-    banner(f"draft append + rollback storage={dtype} S={S} W={Wn} lengths [{lo}, {hi}]")
-    gen = torch.Generator().manual_seed(900 + S * 31 + Wn + lo)
-    B, Hkv, D, k = 9, 2, 64, 4
+    _draft_case(dtype, S, Wn, lo, hi)
+
+
+# the element-by-element path (head dim not a multiple of 4; misaligned inputs)
+@pytest.mark.parametrize("dtype", ["bf16", "fp8", "f32"])
+@pytest.mark.parametrize("D,offset", [(30, 0), (64, 1)])
+def test_draft_append_and_rollback_scalar_path_match_oracle(dtype, D, offset):
+    _draft_case(dtype, 4, 16, 1, 40, D=D, offset=offset)
+
+
+def _draft_case(dtype, S, Wn, lo, hi, D=64, offset=0):
+    banner(f"draft append + rollback storage={dtype} S={S} W={Wn} lengths [{lo}, {hi}] D={D} "
+           f"input offset={offset}")
+    gen = torch.Generator().manual_seed(900 + S * 31 + Wn + lo + D + offset)
+    B, Hkv, k = 9, 2, 4
     base = torch.randint(lo, hi + 1, (B,), generator=gen, dtype=torch.int32)
     offs = torch.randint(0, max(Wn, 1), (B,), generator=gen, dtype=torch.int32)
     offs[0] = -7 if Wn > 0 else 0            # reduced modulo W on the device
@@ -152,7 +188,8 @@ def test_draft_append_and_rollback_match_oracle(dtype, S, Wn, lo, hi):
     for s in range(k):
         kn, vn = news[s]
         lens = (base + s + 1).to(DEV)
-        spire.draft_append(sink, ring, kn.to(DEV), vn.to(DEV), lens, offs.to(DEV), S, Wn, spk[s], spv[s])
+        spire.draft_append(sink, ring, _on_device(kn, offset), _on_device(vn, offset), lens, offs.to(DEV),
+                           S, Wn, spk[s], spv[s])
         KU.draft_append(*host, kn.numpy(), vn.numpy(), (base + s + 1).numpy(), offs_np, S, Wn, dtype,
                         None if ks is None else ks.cpu().numpy(), None if vs is None else vs.cpu().numpy(),
                         hspk[s], hspv[s])
