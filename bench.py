@@ -568,8 +568,8 @@ def main():
         print(kernel_source_hash())
         return
     if a.gpus != 1:
-        print(f"bench.py measures one GPU only (asked for --gpus {a.gpus}); the multi-GPU sharding "
-              "of this path is described in DESIGN.md and is not run.", file=sys.stderr)
+        print(f"bench.py measures one GPU only (asked for --gpus {a.gpus}); this path is not run "
+              "sharded over several GPUs.", file=sys.stderr)
         sys.exit(2)
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
