@@ -38,16 +38,28 @@ namespace spire {
 template <bool FP8, int NB, int MODE>
 __global__ __launch_bounds__(256, 1) void mfma_partial_kernel(Problem p, Plan pl) {
     static_assert(NB >= 1 && NB <= 2, "more than 32 rows go to the LDS-staged kernel");
+    __shared__ int32_t s_pre[kPlanMaxB + 1];
+    __shared__ int32_t s_sum[64 * kMfmaWavesPerWG];
+    // the partition: no separate plan launch (its few microseconds per call
+    // were a tenth of a short draft step)
+    plan_in_kernel<64 * kMfmaWavesPerWG>(p, pl, s_pre, s_sum);
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
     const int wid = __builtin_amdgcn_readfirstlane(blockIdx.x * kMfmaWavesPerWG + wave);
     if (wid >= pl.workers) return;
-    const int64_t T = (int64_t)uload(pl.prefix, p.B) * pl.units;
+    const int64_t T = (int64_t)s_pre[p.B] * pl.units;
     int64_t pos = worker_begin(wid, T, pl.workers);
     const int64_t end = worker_begin(wid + 1, T, pl.workers);
-    if (pos >= end) return;
-    int seg = uload(pl.wstart, 2 * wid);
-    int tile = uload(pl.wstart, 2 * wid + 1);
+    if (pos >= end) {
+        if (lane == 0) pl.wstart[2 * wid] = -1;
+        return;
+    }
+    int seg, tile;
+    locate(s_pre, p.B, pl.units, pos, seg, tile);
+    if (lane == 0) {  // recorded like the plan kernel's output
+        pl.wstart[2 * wid] = seg;
+        pl.wstart[2 * wid + 1] = tile;
+    }
     const int64_t begin = pos;
 
     QFrag<NB, false> qf;
@@ -55,7 +67,7 @@ __global__ __launch_bounds__(256, 1) void mfma_partial_kernel(Problem p, Plan pl
     while (pos < end) {
         const int b = seg / pl.units;
         const int h = seg - b * pl.units;
-        const int span = uload(pl.prefix, b + 1) - uload(pl.prefix, b);
+        const int span = s_pre[b + 1] - s_pre[b];
         const int tiles_b = span - pl.seg_cost;
         const int64_t left = end - pos;
         const int te = left < (int64_t)(span - tile) ? tile + (int)left : span;
@@ -66,7 +78,7 @@ __global__ __launch_bounds__(256, 1) void mfma_partial_kernel(Problem p, Plan pl
             continue;
         }
         const int t1 = te < tiles_b ? te : tiles_b;
-        const int n = uload(pl.nkeys, b);
+        const int n = effective_keys(p, b);
 
         const SegAddr a = make_seg_addr<MODE>(p, b, h, n);
         SoftmaxState<NB, false> st;

@@ -385,6 +385,62 @@ __device__ __forceinline__ void compute_tile(TileRegs<FP8> &T, const QFrag<NB, Q
     }
 }
 
+// ---- the partition computed inside an attention kernel --------------------------
+// Every workgroup of THREADS threads computes the prefix sums of the
+// (tiles + phantom positions) of all sequences into s_pre[0..B] (the plan
+// kernel's arithmetic); workgroup 0 also stores the key counts and prefix sums
+// in the workspace, where the combine reads them.  Ends with a barrier.
+template <int THREADS>
+__device__ __forceinline__ void plan_in_kernel(const Problem &p, const Plan &pl, int32_t *s_pre,
+                                               int32_t *s_sum) {
+    const int tid = threadIdx.x, B = p.B;
+    const int per = (B + THREADS - 1) / THREADS;
+    const int b0 = tid * per;
+    const int b1 = b0 + per < B ? b0 + per : B;
+    const bool store = blockIdx.x == 0;
+    int local = 0;
+    for (int b = b0; b < b1; ++b) {
+        const int n = effective_keys(p, b);
+        if (store) pl.nkeys[b] = n;
+        const int span = (n > 0 ? (n + pl.tile - 1) / pl.tile : 1) + pl.seg_cost;
+        s_pre[b] = span;
+        local += span;
+    }
+    s_sum[tid] = local;
+    __syncthreads();
+    for (int off = 1; off < THREADS; off <<= 1) {  // inclusive scan of the per-thread sums
+        const int v = tid >= off ? s_sum[tid - off] : 0;
+        __syncthreads();
+        s_sum[tid] += v;
+        __syncthreads();
+    }
+    int run = s_sum[tid] - local;
+    for (int b = b0; b < b1; ++b) {
+        const int span = s_pre[b];
+        s_pre[b] = run;
+        if (store) pl.prefix[b] = run;
+        run += span;
+    }
+    if (tid == THREADS - 1) {
+        s_pre[B] = s_sum[THREADS - 1];
+        if (store) pl.prefix[B] = s_sum[THREADS - 1];
+    }
+    __syncthreads();
+}
+
+// (segment, tile) holding flattened position x (0 <= x < T) under prefix sums s_pre
+__device__ __forceinline__ void locate(const int32_t *s_pre, int B, int units, int64_t x, int &seg, int &tile) {
+    int lo = 0, hi = B - 1;  // last b with units * s_pre[b] <= x
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if ((int64_t)s_pre[mid] * units <= x) lo = mid; else hi = mid - 1;
+    }
+    const int span = s_pre[lo + 1] - s_pre[lo];
+    const int64_t rel = x - (int64_t)s_pre[lo] * units;
+    seg = lo * units + (int)(rel / span);
+    tile = (int)(rel % span);
+}
+
 // ---- per-segment setup and finalisation ---------------------------------------
 
 template <int MODE>

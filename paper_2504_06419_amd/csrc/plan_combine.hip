@@ -17,24 +17,6 @@
 namespace spire {
 
 constexpr int kPlanThreads = 1024;
-constexpr int kPlanMaxB = 8192;
-
-__device__ __forceinline__ int effective_keys(const Problem &p, int b) {
-    int n = p.lens[b];
-    if (!p.draft) {
-        int64_t cap = p.kv.page_size > 0 ? (int64_t)p.kv.max_blocks * p.kv.page_size
-                                         : (int64_t)p.kv.capacity;
-        if (cap > INT32_MAX) cap = INT32_MAX;
-        n = n < 0 ? 0 : (n > cap ? (int)cap : n);
-    } else {
-        const int m = n < 0 ? 0 : n;
-        const int ns = m < p.S ? m : p.S;
-        int nr = m - p.S;
-        nr = nr < 0 ? 0 : (nr > p.W ? p.W : nr);
-        n = ns + nr;
-    }
-    return n;
-}
 
 __global__ __launch_bounds__(kPlanThreads) void plan_kernel(Problem p, Plan pl) {
     __shared__ int32_t prefix[kPlanMaxB + 1];

@@ -246,8 +246,13 @@ spire_status run(Problem &p, bool use_mfma, void *workspace, size_t ws_bytes, hi
     pl.part_lse = reinterpret_cast<float *>(ws + L.part_lse);
     pl.part_o = reinterpret_cast<float *>(ws + L.part_o);
 
-    hipError_t e = timed_launch(0, stream, launch_plan, p, pl);
-    if (e != hipSuccess) return fail(SPIRE_ERR_HIP, "plan launch: %s", hipGetErrorString(e));
+    // the register-staged kernel computes the partition itself; the others
+    // read it from the plan kernel's output
+    hipError_t e = hipSuccess;
+    if (!mf || staged) {
+        e = timed_launch(0, stream, launch_plan, p, pl);
+        if (e != hipSuccess) return fail(SPIRE_ERR_HIP, "plan launch: %s", hipGetErrorString(e));
+    }
     if (staged) {
         auto fn = [](const Problem &pp, const Plan &pp2, hipStream_t s) {
             return launch_staged_partial(pp, pp2, (pp.R + 15) / 16, s);

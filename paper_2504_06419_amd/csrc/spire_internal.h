@@ -103,6 +103,28 @@ __device__ __forceinline__ int64_t worker_of(int64_t x, int64_t T, int64_t worke
     return ((x + 1) * workers - 1) / T;
 }
 
+constexpr int kPlanMaxB = 8192;  // sequences per call (the partition's LDS arrays)
+
+// Keys of sequence b the kernels attend to: verify lengths clamped to what
+// the cache descriptor can address, draft lengths to the sinks present plus
+// the valid ring slots.
+__device__ __forceinline__ int effective_keys(const Problem &p, int b) {
+    int n = p.lens[b];
+    if (!p.draft) {
+        int64_t cap = p.kv.page_size > 0 ? (int64_t)p.kv.max_blocks * p.kv.page_size
+                                         : (int64_t)p.kv.capacity;
+        if (cap > INT32_MAX) cap = INT32_MAX;
+        n = n < 0 ? 0 : (n > cap ? (int)cap : n);
+    } else {
+        const int m = n < 0 ? 0 : n;
+        const int ns = m < p.S ? m : p.S;
+        int nr = m - p.S;
+        nr = nr < 0 ? 0 : (nr > p.W ? p.W : nr);
+        n = ns + nr;
+    }
+    return n;
+}
+
 // Row r of KV head h (r in [0, R)) -> element offset of its query/output row
 // in [B, k+1, Hq, D]: rows are ordered (draft index i, head in group hg).
 __device__ __forceinline__ int64_t row_offset(const Problem &p, int b, int h, int r) {
