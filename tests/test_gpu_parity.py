@@ -307,24 +307,32 @@ def test_verify_tp8shard_fp8_B512_k8():
     _check_verify(inp, TOL["fp8"], seq_ids=ids)
 
 
-def test_plan_partition_invariants():
-    """The plan kernel's output read back from the workspace (layout of
-    spire_abi.hip): clamped key counts, prefix sums of tile + phantom positions,
-    worker start points."""
-    banner("plan partition")
-    spec = W.VerifySpec(B=37, Hq=32, Hkv=8, D=128, k=4, ctx_lo=1, ctx_hi=5000, page_size=16)
+# (kv dtype, k, query heads per KV head, phantom positions per segment):
+# bf16 20 rows and fp8 8 rows run the register-staged kernel, which computes
+# the partition itself; fp8 72 rows runs the LDS-staged kernel after the plan
+# kernel.  Phantom positions: the tiles holding 40 KB of K+V (32 keys x 128
+# dims x 2 tensors: 16 KB per bf16 tile, 8 KB per fp8 tile).
+@pytest.mark.parametrize("kv_dtype,k,g,seg_cost", [("bf16", 4, 4, 3), ("fp8", 0, 8, 5), ("fp8", 8, 8, 5)])
+def test_plan_partition_invariants(kv_dtype, k, g, seg_cost):
+    """The partition read back from the workspace (layout of spire_abi.hip):
+    clamped key counts, prefix sums of tile + phantom positions, worker start
+    points."""
+    banner(f"plan partition: {kv_dtype} k={k} g={g}")
+    Hkv = 8
+    spec = W.VerifySpec(B=37, Hq=g * Hkv, Hkv=Hkv, D=128, k=k, ctx_lo=1, ctx_hi=5000, page_size=16,
+                        kv_dtype=kv_dtype)
     inp = W.make_verify_inputs(spec, 14, device=DEV)
     cap = inp.block_table.shape[1] * 16
     lens = inp.kv_lens.clone()
     lens[3] = 0
     lens[5] = cap + 100
     inp.kv_lens = lens
-    ws = spire.workspace(spire.verify_workspace_size(37, 32, 8, 128, 4))
+    ws = spire.workspace(spire.verify_workspace_size(37, g * Hkv, Hkv, 128, k))
     ws.fill_(0xAB)
     run_verify(inp, ws=ws)
     raw = ws.cpu()
     al = lambda x: (x + 255) // 256 * 256
-    B, tile, units = 37, 32, 8
+    B, tile, units = 37, 32, Hkv
     nkeys = raw[0:4 * B].view(torch.int32)
     o1 = al(4 * B)
     prefix = raw[o1:o1 + 4 * (B + 1)].view(torch.int32)
@@ -332,9 +340,6 @@ def test_plan_partition_invariants():
     workers = torch.cuda.get_device_properties(0).multi_processor_count * 4
     wstart = raw[o2:o2 + 8 * workers].view(torch.int32).view(-1, 2)
     assert nkeys.tolist() == torch.clamp(lens.cpu(), 0, cap).tolist()
-    # every segment also owns phantom positions for its fixed cost: the
-    # equivalent of 40 KB of tiles, 3 tiles of 32 bf16 keys x 128 dims x (K, V)
-    seg_cost = 3
     tiles = [max(1, (n + tile - 1) // tile) + seg_cost for n in nkeys.tolist()]
     assert prefix.tolist() == [sum(tiles[:b]) for b in range(B + 1)]
     T = prefix[B].item() * units
