@@ -80,23 +80,37 @@ hipError_t launch_plan(const Problem &p, const Plan &pl, hipStream_t st) {
     return hipGetLastError();
 }
 
-// Workgroup (segment, row chunk): a segment's rows are split into gridDim.y
-// chunks, one thread per 4 output elements; workgroups of segments that one
-// worker covered return at once.  The partial slot of every worker covering the segment (or -1 for a
-// worker with an empty range) is worked out once per workgroup into LDS, so
+// Merge of the segments several workers shared.  The grid is either one
+// workgroup per (segment, row chunk) -- workgroups of segments one worker
+// covered return at once -- or, when segments outnumber workers, one per
+// (worker w, row chunk): w merges the segment it starts inside of when it is
+// the first worker to start inside that segment's tiles (every split segment
+// has exactly one such worker), so no workgroup is spent on unsplit segments.
+// The segment's rows are split into gridDim.y chunks, one thread per 4 output
+// elements.  The partial slot of every worker covering the segment (or -1 for
+// a worker with an empty range) is worked out once per workgroup into LDS, so
 // the merge loops do no 64-bit divisions.
+template <bool PER_WORKER>
 __global__ __launch_bounds__(256) void combine_kernel(Problem p, Plan pl) {
     __shared__ int32_t s_slot[kCombineMaxWorkers];
-    const int seg = blockIdx.x;
+    int seg = blockIdx.x, tile0 = 0;
+    if (PER_WORKER) {
+        seg = pl.wstart[2 * blockIdx.x];
+        if (seg < 0) return;  // empty range
+        tile0 = pl.wstart[2 * blockIdx.x + 1];
+    }
     const int b = seg / pl.units, u = seg - (seg / pl.units) * pl.units;
     const int span = pl.prefix[b + 1] - pl.prefix[b];  // tiles + phantom positions
     const int tiles = span - pl.seg_cost;
+    if (PER_WORKER && (tile0 == 0 || tile0 >= tiles)) return;  // starts at the first tile or past the last
     const int64_t T = (int64_t)pl.prefix[p.B] * pl.units;
     const int64_t start = (int64_t)pl.prefix[b] * pl.units + (int64_t)u * span;
     // the workers whose ranges hold the segment's tiles (phantoms are not read)
     const int64_t wlo = worker_of(start, T, pl.workers);
     const int64_t whi = worker_of(start + tiles - 1, T, pl.workers);
     if (wlo == whi) return;
+    // workers wlo+1 .. whi start inside the tiles; the first non-empty one merges
+    if (PER_WORKER && worker_begin(blockIdx.x, T, pl.workers) != worker_begin(wlo + 1, T, pl.workers)) return;
 
     const int nw = (int)(whi - wlo + 1);  // <= workers <= kCombineMaxWorkers
     const int64_t begin_lo = worker_begin(wlo, T, pl.workers);
@@ -156,18 +170,21 @@ __global__ __launch_bounds__(256) void combine_kernel(Problem p, Plan pl) {
 }
 
 hipError_t launch_combine(const Problem &p, const Plan &pl, hipStream_t st) {
-    const int64_t segs = (int64_t)p.B * pl.units;
-    if (segs == 0) return hipSuccess;
+    if ((int64_t)p.B * pl.units == 0) return hipSuccess;
     if (pl.workers > kCombineMaxWorkers) return hipErrorInvalidValue;
-    // split the rows of a segment over up to one workgroup per 256 outputs
-    // while there are few segments (at most ~4096 workgroups in all: most of
-    // them belong to segments that need no merge and return at once, and more
-    // measured slower at 4096 segments)
-    const int rpw = 256 / (p.D / 4);
+    const int64_t segs = (int64_t)p.B * pl.units;
+    const int rpw = 256 / (p.D / 4);  // rows per chunk: one thread per 4 outputs
     const int64_t want = (pl.rows + rpw - 1) / rpw;
-    const int64_t room = segs >= 4096 ? 1 : 4096 / segs;
-    const unsigned chunks = (unsigned)(want < room ? want : room);
-    hipLaunchKernelGGL(combine_kernel, dim3((unsigned)segs, chunks), dim3(256), 0, st, p, pl);
+    if (segs > pl.workers) {  // at most one split segment per worker start
+        hipLaunchKernelGGL(combine_kernel<true>, dim3((unsigned)pl.workers, (unsigned)want), dim3(256), 0, st, p,
+                           pl);
+    } else {
+        // one workgroup per segment, its rows split while that keeps the grid
+        // within ~4096 workgroups (more measured slower)
+        const int64_t room = segs >= 4096 ? 1 : 4096 / segs;
+        hipLaunchKernelGGL(combine_kernel<false>, dim3((unsigned)segs, (unsigned)(want < room ? want : room)),
+                           dim3(256), 0, st, p, pl);
+    }
     return hipGetLastError();
 }
 
