@@ -114,8 +114,9 @@ size_t spire_verify_workspace_size(int32_t B, int32_t Hq, int32_t Hkv, int32_t D
  *            causal mask).  n_b >= k+1 for a full result; smaller values are
  *            legal (rows with no visible key return zeros, lse = -inf); values
  *            above the cache capacity are clamped to it.
- *   sizes    B >= 0, Hkv >= 1, Hq % Hkv == 0, D in {64, 128}, 0 <= k <= 15,
- *            (k+1) * Hq / Hkv <= 128.
+ *   sizes    0 <= B <= 8192, Hkv >= 1, Hq % Hkv == 0, D in {64, 128},
+ *            0 <= k <= 15, (k+1) * Hq / Hkv <= 128 (SPIRE_ERR_UNSUPPORTED
+ *            beyond these limits).
  *   sm_scale softmax scale (usually 1/sqrt(D)); finite and > 0, else
  *            SPIRE_ERR_INVALID_ARG.
  *   out      [B, k+1, Hq, D] contiguous, out_dtype SPIRE_F32 or SPIRE_BF16.

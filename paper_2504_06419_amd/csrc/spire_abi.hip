@@ -195,7 +195,7 @@ spire_status common_checks(const void *q, int q_dtype, int B, int Hq, int Hkv, i
         return fail(SPIRE_ERR_UNSUPPORTED, "out_dtype must be F32 or BF16");
     if (B > 0 && (q == nullptr || out == nullptr)) return fail(SPIRE_ERR_INVALID_ARG, "q or out is NULL");
     if (B > 0 && workspace == nullptr) return fail(SPIRE_ERR_WORKSPACE, "workspace is NULL");
-    if (B > 8192) return fail(SPIRE_ERR_UNSUPPORTED, "B must be <= 8192 (got %d)", B);
+    if (B > kPlanMaxB) return fail(SPIRE_ERR_UNSUPPORTED, "B must be <= %d (got %d)", kPlanMaxB, B);
     if (!aligned16(q) || !aligned16(out)) return fail(SPIRE_ERR_INVALID_ARG, "q and out must be 16-byte aligned");
     if (((uintptr_t)workspace & 255u) != 0) return fail(SPIRE_ERR_WORKSPACE, "workspace must be 256-byte aligned");
     return SPIRE_OK;
