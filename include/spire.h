@@ -124,6 +124,10 @@ size_t spire_verify_workspace_size(int32_t B, int32_t Hq, int32_t Hkv, int32_t D
  *   workspace >= spire_verify_workspace_size(B, Hq, Hkv, D, k) bytes of device
  *            memory, 256-byte aligned; its contents need no initialisation.
  * Supported storage: KV f32, bf16 or fp8 (fp8 needs k_scale and v_scale).
+ * Non-finite values in the visible keys act as in the definition: a NaN key
+ * or value, or a key whose score is +inf, makes the rows that see it NaN
+ * (output and lse); a score of -inf weighs zero.  Storage outside the visible
+ * keys never influences a result, whatever it holds.
  */
 spire_status spire_verify_attn(const void *q, int32_t q_dtype, const spire_kv *kv,
                                const int32_t *kv_lens, int32_t B, int32_t Hq, int32_t Hkv,
@@ -153,6 +157,7 @@ size_t spire_draft_workspace_size(int32_t B, int32_t Hq, int32_t Hkv, int32_t D)
  *   ring_offset [B] int32, reduced modulo W on the device.
  *   sizes    S >= 0, W >= 0, S + W >= 1, other sizes as for verify with k = 0.
  *   out      [B, Hq, D]; lse [B, Hq] or NULL; workspace as for verify.
+ * Non-finite values in visible positions act as for verify.
  */
 spire_status spire_draft_sparse_attn(const void *q, int32_t q_dtype, const spire_kv *sink,
                                      const spire_kv *ring, const int32_t *seq_lens,

@@ -206,8 +206,9 @@ __global__ __launch_bounds__(64) void generic_partial_kernel(Problem p, Plan pl)
         for (int r = 0; r < RB; ++r) {
             const float L = wave_sum(l[r]);
             if (r0 + r >= p.R) continue;
-            const float inv = L > 0.f ? 1.f / L : 0.f;
-            const float lse2 = L > 0.f ? m[r] + log2f(L) : -INFINITY;
+            // L == 0: no visible key; L NaN: a NaN key or a +inf score was visible
+            const float inv = L > 0.f ? 1.f / L : (L == 0.f ? 0.f : L);
+            const float lse2 = L > 0.f ? m[r] + log2f(L) : (L == 0.f ? -INFINITY : L);
             if (whole) {
                 const int64_t off = row_offset(p, b, h, r0 + r);
 #pragma unroll

@@ -550,8 +550,10 @@ __device__ __forceinline__ void end_rows(const Problem &p, const Plan &pl, Softm
         }
         const int r = 16 * (rb0 + nb) + n16;
         if (r >= p.R) continue;
-        const float inv = l > 0.f ? vs / l : 0.f;
-        const float lse2 = l > 0.f ? st.msub[nb] + log2f(l) : -INFINITY;
+        // l == 0: no visible key (zeros, lse -inf); l NaN: a NaN key or a +inf
+        // score was visible, and the row is NaN as the definition has it
+        const float inv = l > 0.f ? vs / l : (l == 0.f ? 0.f : l);
+        const float lse2 = l > 0.f ? st.msub[nb] + log2f(l) : (l == 0.f ? -INFINITY : l);
         if (whole) {
             const int64_t off = row_offset(p, b, h, r) + 32 * j;
 #pragma unroll

@@ -133,14 +133,19 @@ __global__ __launch_bounds__(256) void combine_kernel(Problem p, Plan pl) {
     const int rhi = rlo + rpc < nrows ? rlo + rpc : nrows;
     for (int idx = threadIdx.x; idx < (rhi - rlo) * d4n; idx += blockDim.x) {
         const int r = rlo + idx / d4n, d4 = idx - (idx / d4n) * d4n;
+        // a NaN partial (a NaN key or a +inf score in that part) makes the row NaN
         float M = -INFINITY;
+        bool nan = false;
         for (int i = 0; i < nw; ++i) {
             const int slot = s_slot[i];
-            if (slot >= 0) M = fmaxf(M, pl.part_lse[(int64_t)slot * pl.rows + r]);
+            if (slot < 0) continue;
+            const float lp = pl.part_lse[(int64_t)slot * pl.rows + r];
+            if (lp != lp) nan = true;
+            else M = fmaxf(M, lp);
         }
-        float L = 0.f;
-        float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (M != -INFINITY) {
+        float L = nan ? __builtin_nanf("") : 0.f;
+        float4 acc = make_float4(L, L, L, L);
+        if (!nan && M != -INFINITY) {
             for (int i = 0; i < nw; ++i) {
                 const int slot = s_slot[i];
                 if (slot < 0) continue;
@@ -152,7 +157,7 @@ __global__ __launch_bounds__(256) void combine_kernel(Problem p, Plan pl) {
                 acc.x += wgt * o.x; acc.y += wgt * o.y; acc.z += wgt * o.z; acc.w += wgt * o.w;
             }
         }
-        const float inv = L > 0.f ? 1.f / L : 0.f;
+        const float inv = L > 0.f ? 1.f / L : (L == 0.f ? 0.f : L);
         const int64_t off = row_offset(p, b, h, r0 + r) + 4 * d4;
         if (p.out_dtype == SPIRE_BF16) {
             uint16_t *o = reinterpret_cast<uint16_t *>(p.out) + off;
@@ -165,7 +170,7 @@ __global__ __launch_bounds__(256) void combine_kernel(Problem p, Plan pl) {
         }
         if (d4 == 0 && p.lse != nullptr)
             p.lse[lse_index(p, b, h, r0 + r)] = L > 0.f ? (M + log2f(L)) * 0.69314718055994531f
-                                                         : -INFINITY;
+                                                         : (L == 0.f ? -INFINITY : L);
     }
 }
 
