@@ -3,7 +3,8 @@
 
 A step is one pass of the hot path over one synthetic batch already resident
 in HBM:
-  * verify workloads: plan -> verify partial attention -> combine;
+  * verify workloads: verify partial attention -> combine (a separate plan
+    launch first where the LDS-staged or generic kernel serves the call);
   * draft workloads:  the k sequential draft-step attention calls;
   * the fp8 round:    k draft-step calls, then the verify call.
 The default workload is the variable-length paged bf16 verify batch (B=256,
