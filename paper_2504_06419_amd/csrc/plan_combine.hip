@@ -1,17 +1,20 @@
 // plan_combine.hip -- work partition (plan) and split-segment merge (combine).
 //
 // The plan reads the per-sequence lengths on the device, clamps them to what
-// the cache descriptors can address, cuts every sequence into key tiles and
-// assigns each worker an equal share of all tiles (see spire_internal.h).  It
-// runs as one workgroup; everything it produces stays in the caller's
-// workspace.
+// the cache descriptors can address, cuts every sequence into key tiles (plus
+// the phantom positions of each segment) and assigns each worker an equal
+// share of all positions (see spire_internal.h).  It runs as one workgroup
+// ahead of the LDS-staged and generic kernels; the register-staged kernel
+// computes the same partition itself (plan_in_kernel, mfma_common.h).
+// Everything it produces stays in the caller's workspace.
 //
 // The combine merges the partial results of a segment that several workers
 // shared: with partials (o_p, lse_p) in base 2,
 //   M = max_p lse_p,  w_p = 2^(lse_p - M),  out = sum_p w_p o_p / sum_p w_p,
 //   lse = (M + log2 sum_p w_p) * ln 2,
 // the log-sum-exp identity that makes attention over a union of disjoint key
-// sets equal to a weighted merge of attention over each set.
+// sets equal to a weighted merge of attention over each set.  A NaN partial
+// (a NaN key or a +inf score in that part) makes the merged row NaN.
 #include "spire_internal.h"
 
 namespace spire {
