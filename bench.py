@@ -420,12 +420,19 @@ KERNEL_SOURCES = ["paper_2504_06419_amd/csrc/attn_mfma.hip",
 
 
 def kernel_source_hash() -> str:
-    """sha256 over the sources of the measured kernels; recorded HBM traffic is
-    reported only while the kernels are the ones the counters were taken on."""
+    """sha256 over the code of the measured kernels' sources (line comments and
+    blank lines left out, so that editing a comment keeps the record valid);
+    recorded HBM traffic is reported only while the kernels are the ones the
+    counters were taken on."""
     import hashlib
+    import re
     h = hashlib.sha256()
     for f in KERNEL_SOURCES:
-        h.update(open(os.path.join(ROOT, f), "rb").read())
+        text = open(os.path.join(ROOT, f), encoding="utf-8").read()
+        if not f.endswith(".py"):
+            text = re.sub(r"//[^\n]*", "", text)
+        lines = [ln.rstrip() for ln in text.splitlines()]
+        h.update("\n".join(ln for ln in lines if ln).encode())
     return h.hexdigest()
 
 
