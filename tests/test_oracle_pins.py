@@ -328,3 +328,33 @@ def test_empty_visible_set_outputs_zero():
     lens = torch.zeros_like(inp.kv_lens)
     o, l = O.verify(inp.q, inp.k_cache, inp.v_cache, lens, 2, inp.sm_scale)
     assert np.all(o == 0.0) and np.all(np.isneginf(l))
+
+
+@pytest.mark.parametrize("ps", [0, 4])
+def test_nonfinite_visible_keys_match_brute_force(ps):
+    """A NaN key or value, or a key scoring +inf, inside the visible range
+    makes the rows that see it NaN (output and lse) in the C oracle exactly as
+    in the Python brute force; a -inf score weighs zero."""
+    inp = vin(B=3, Hq=4, Hkv=2, D=8, k=2, lo=10, hi=10, dtype="f32", ps=ps, seed=21)
+    # logical position 4 of sequence 1 (visible to every query) and position 6
+    # of sequence 2; the stored copy is located through the same layout
+    def put(tensor_s, tensor_l, b, h, p, d, val):
+        tensor_l[b, h, p, d] = val
+        if ps:
+            page = int(inp.block_table[b, p // ps])
+            tensor_s[page, h, p % ps, d] = val
+        else:
+            tensor_s[b, h, p, d] = val
+    put(inp.k_cache, inp.logical_k, 1, 0, 4, 3, float("nan"))
+    put(inp.v_cache, inp.logical_v, 2, 1, 6, 5, float("nan"))
+    put(inp.k_cache, inp.logical_k, 0, 1, 2, 0, float("inf"))
+    o, l = oracle_verify(inp)
+    with np.errstate(invalid="ignore"):  # inf - inf on purpose
+        bo, bl = brute.verify(inp.q, inp.logical_k, inp.logical_v, inp.kv_lens.tolist(), inp.spec.k,
+                              inp.sm_scale)
+    assert np.isnan(l).any() and np.isfinite(l).any()
+    assert np.array_equal(np.isnan(o), np.isnan(bo)) and np.array_equal(np.isnan(l), np.isnan(bl))
+    fin, lfin = np.isfinite(bo), np.isfinite(bl)
+    assert np.array_equal(np.isfinite(o), fin) and np.array_equal(np.isfinite(l), lfin)
+    assert np.max(np.abs(o[fin] - bo[fin])) <= TOL
+    assert np.max(np.abs(l[lfin] - bl[lfin])) <= TOL
