@@ -289,9 +289,10 @@ spire_status spire_feedback_memory(const void *x, int32_t x_dtype, const float *
  * Streaming-read probe (a measurement aid, not a step of the method): reads
  * the `bytes` bytes at device pointer `buf` once with 16-byte nontemporal
  * loads, as a plain streaming kernel does, and writes an XOR fold of what it
- * read to the device array `sink`, which must hold
- * SPIRE_HBM_PROBE_SINK_WORDS words (every word is written; the XOR of all of
- * them equals the XOR of every 32-bit word of the buffer).  Its duration gives
+ * read to the device array `sink` of `sink_words` words, which must be at
+ * least SPIRE_HBM_PROBE_SINK_WORDS (else SPIRE_ERR_INVALID_ARG); the first
+ * SPIRE_HBM_PROBE_SINK_WORDS words are written, and their XOR equals the XOR
+ * of every 32-bit word of the buffer.  Its duration gives
  * the HBM read rate this device reaches in practice, the ceiling the
  * attention kernels are compared against beside the 8 TB/s specification.
  *   buf   16-byte aligned, bytes a multiple of 16 (0 is allowed: nothing read,
@@ -301,7 +302,8 @@ spire_status spire_feedback_memory(const void *x, int32_t x_dtype, const float *
  * records.
  */
 #define SPIRE_HBM_PROBE_SINK_WORDS 2048
-spire_status spire_hbm_read_probe(const void *buf, size_t bytes, uint32_t *sink, hipStream_t stream);
+spire_status spire_hbm_read_probe(const void *buf, size_t bytes, uint32_t *sink, size_t sink_words,
+                                  hipStream_t stream);
 
 /* Human-readable name of a status code (static string, never NULL). */
 const char *spire_status_string(spire_status status);

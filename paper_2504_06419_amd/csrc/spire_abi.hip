@@ -599,9 +599,12 @@ spire_status spire_feedback_memory(const void *x, int32_t x_dtype, const float *
     return SPIRE_OK;
 }
 
-spire_status spire_hbm_read_probe(const void *buf, size_t bytes, uint32_t *sink, hipStream_t stream) {
+spire_status spire_hbm_read_probe(const void *buf, size_t bytes, uint32_t *sink, size_t sink_words,
+                                  hipStream_t stream) {
     g_err[0] = '\0';
     if (sink == nullptr || (bytes > 0 && buf == nullptr)) return fail(SPIRE_ERR_INVALID_ARG, "buf or sink is NULL");
+    if (sink_words < SPIRE_HBM_PROBE_SINK_WORDS)
+        return fail(SPIRE_ERR_INVALID_ARG, "sink holds %zu words, needs %d", sink_words, SPIRE_HBM_PROBE_SINK_WORDS);
     if (((uintptr_t)buf & 15u) != 0 || bytes % 16 != 0)
         return fail(SPIRE_ERR_INVALID_ARG, "buf must be 16-byte aligned and bytes a multiple of 16");
     if (((uintptr_t)sink & 3u) != 0) return fail(SPIRE_ERR_INVALID_ARG, "sink must be 4-byte aligned");

@@ -95,7 +95,7 @@ def load(path: Optional[str] = None):
     L.spire_set_kernel_variant.restype = C.c_int
     L.spire_set_kernel_variant.argtypes = [i32]
     L.spire_hbm_read_probe.restype = C.c_int
-    L.spire_hbm_read_probe.argtypes = [vp, sz, vp, vp]
+    L.spire_hbm_read_probe.argtypes = [vp, sz, vp, sz, vp]
     L.spire_timing_enable.restype = C.c_int
     L.spire_timing_enable.argtypes = [i32]
     L.spire_timing_collect.restype = i32
@@ -290,9 +290,9 @@ def hbm_read_probe(buf: torch.Tensor, sink: Optional[torch.Tensor] = None) -> to
     assert buf.is_contiguous() and buf.is_cuda
     if sink is None:
         sink = torch.empty((HBM_PROBE_SINK_WORDS,), dtype=torch.int32, device=buf.device)
-    assert sink.dtype == torch.int32 and sink.numel() >= HBM_PROBE_SINK_WORDS
+    assert sink.dtype == torch.int32 and sink.is_cuda
     _check(load().spire_hbm_read_probe(buf.data_ptr(), buf.numel() * buf.element_size(),
-                                       sink.data_ptr(), _stream()))
+                                       sink.data_ptr(), sink.numel(), _stream()))
     return sink
 
 

@@ -303,8 +303,8 @@ def test_feedback_memory_empty_is_a_no_op():
     assert _fm(d=0, x=None, w=None, m=None) == OK
 
 
-def _probe(buf=FAKE, nbytes=1 << 20, sink=FAKE):
-    return spire.load().spire_hbm_read_probe(buf, nbytes, sink, None)
+def _probe(buf=FAKE, nbytes=1 << 20, sink=FAKE, words=spire.HBM_PROBE_SINK_WORDS):
+    return spire.load().spire_hbm_read_probe(buf, nbytes, sink, words, None)
 
 
 @pytest.mark.parametrize("kw", [
@@ -313,6 +313,7 @@ def _probe(buf=FAKE, nbytes=1 << 20, sink=FAKE):
     dict(buf=FAKE + 8),
     dict(nbytes=(1 << 20) + 4),
     dict(sink=FAKE + 2),
+    dict(words=spire.HBM_PROBE_SINK_WORDS - 1),
 ])
 def test_hbm_read_probe_rejects_invalid_arguments(kw):
     assert _probe(**kw) == INVALID
