@@ -163,9 +163,12 @@ hipError_t launch_generic_partial(const Problem &p, const Plan &pl, hipStream_t 
 hipError_t launch_staged_partial(const Problem &p, const Plan &pl, int nb, hipStream_t st);
 // LDS-staged kernel: waves per worker (a workgroup), waves per SIMD, and the
 // workers of a launch (at most 4 per CU, like the register-staged kernel, so
-// one workspace size serves both).
-constexpr int staged_waves(int nb) { return nb <= 2 ? 1 : 2; }
-constexpr int staged_wps(bool fp8, int nb) { return fp8 && nb > 2 ? 2 : 1; }
+// one workspace size serves both).  fp8 with 5 row blocks (72-80 rows): one
+// wave holds every row block (accumulators in VGPRs, query fragments and
+// spills in AGPRs), so each fp8 tile is converted once and no workgroup
+// barrier orders the stage ring.
+constexpr int staged_waves(bool fp8, int nb) { return nb <= 2 || (fp8 && nb == 5) ? 1 : 2; }
+constexpr int staged_wps(bool fp8, int nb) { return fp8 && nb > 2 && nb < 5 ? 2 : 1; }
 int staged_workers(int cus, int nb, bool fp8);
 hipError_t launch_combine(const Problem &p, const Plan &pl, hipStream_t st);
 hipError_t launch_hbm_read(const void *buf, int64_t bytes, uint32_t *sink, hipStream_t st);
