@@ -202,8 +202,9 @@ spire_status common_checks(const void *q, int q_dtype, int B, int Hq, int Hkv, i
 }
 
 // Kernel family for a matrix-core eligible request: LDS-staged for more than
-// 32 rows (rows split over two waves, deep stage ring), register-staged
-// otherwise; the variant setting can force either.
+// 32 rows (deep stage ring; the row blocks on two waves, or all five fp8
+// blocks on one), register-staged otherwise; the variant setting can force
+// either.
 bool use_staged(const Problem &p) {
     const int nb = (p.R + 15) / 16;
     if (nb > 2) return true;  // the register-staged kernel holds at most 32 rows
