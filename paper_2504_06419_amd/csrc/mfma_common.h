@@ -11,6 +11,9 @@
 //     so P never leaves its lane; row m of dim block mb' is head dim 8m + mb',
 //     so lane l needs dims 8 n16 .. 8 n16 + 7 of keys 4t + j, transposes those
 //     8 keys x 8 dims in registers and owns output dims 32j .. 32j + 31.
+//     The LDS-staged fp8 kernel instead reads V^T transposed from LDS: row m
+//     of dim block mb' is head dim 16 mb' + m, and lane l owns output dims
+//     16 mb' + 4j .. 16 mb' + 4j + 3 of every block mb'.
 // fp8 (OCP e4m3fn) K/V are converted to bf16 in registers (exact); the
 // per-head K scale is folded into the softmax scale, the V scale into the
 // final normalisation.
@@ -252,7 +255,10 @@ template <int NB> struct QFrag<NB, true> {
     __device__ __forceinline__ u32x4 get(int nb, int c, int lane) const { return lds[(nb * 4 + c) * 64 + lane]; }
 };
 
-template <bool FP8, int NB, bool QLDS, bool LS>
+// VTR: T.v[mb] already holds the V^T operand of dim block mb in fp8 (element t
+// = key 4t + j of dim 16 mb + n16, from a transposing LDS read); the output
+// dims of block mb are then 16 mb .. 16 mb + 15 instead of 8 m + mb.
+template <bool FP8, int NB, bool QLDS, bool LS, bool VTR = false>
 __device__ __forceinline__ void compute_tile(TileRegs<FP8> &T, const QFrag<NB, QLDS> &qf,
                                              SoftmaxState<NB, LS> &st, int tile, int n, int full_lim,
                                              float sc, int lane) {
@@ -348,19 +354,36 @@ __device__ __forceinline__ void compute_tile(TileRegs<FP8> &T, const QFrag<NB, Q
 
     // ---- V: keys beyond the segment end are zeroed (storage there may be anything)
     u32x4 vb[8];
+    if constexpr (VTR) {
+        static_assert(FP8, "transposed V operands are read for fp8 only");
+        if (key0 + kMfmaTile > n) {  // uniform: only a segment's last tile
+            // byte t of every operand is key 4t + j
+            uint32_t m0 = 0u, m1 = 0u;
 #pragma unroll
-    for (int t = 0; t < 8; ++t) {
-        if (FP8) {
-            const u32x2 raw = *reinterpret_cast<const u32x2 *>(&T.v[t]);
-            vb[t] = fp8x8_to_bf16x8(raw.x, raw.y);
-        } else {
-            vb[t] = *reinterpret_cast<const u32x4 *>(&T.v[t]);
+            for (int t = 0; t < 4; ++t) {
+                m0 |= (key0 + 4 * t + j < n ? 0xFFu : 0u) << (8 * t);
+                m1 |= (key0 + 4 * (t + 4) + j < n ? 0xFFu : 0u) << (8 * t);
+            }
+#pragma unroll
+            for (int mb = 0; mb < 8; ++mb) T.v[mb] = u32x2{T.v[mb].x & m0, T.v[mb].y & m1};
         }
-    }
-    if (key0 + kMfmaTile > n) {  // uniform: only a segment's last tile
 #pragma unroll
-        for (int t = 0; t < 8; ++t)
-            if (key0 + 4 * t + j >= n) vb[t] = u32x4{0u, 0u, 0u, 0u};
+        for (int mb = 0; mb < 8; ++mb) vb[mb] = fp8x8_to_bf16x8(T.v[mb].x, T.v[mb].y);
+    } else {
+#pragma unroll
+        for (int t = 0; t < 8; ++t) {
+            if (FP8) {
+                const u32x2 raw = *reinterpret_cast<const u32x2 *>(&T.v[t]);
+                vb[t] = fp8x8_to_bf16x8(raw.x, raw.y);
+            } else {
+                vb[t] = *reinterpret_cast<const u32x4 *>(&T.v[t]);
+            }
+        }
+        if (key0 + kMfmaTile > n) {  // uniform: only a segment's last tile
+#pragma unroll
+            for (int t = 0; t < 8; ++t)
+                if (key0 + 4 * t + j >= n) vb[t] = u32x4{0u, 0u, 0u, 0u};
+        }
     }
 
     // ---- O^T += V^T P^T, row sums += 1^T P^T ---------------------------------
@@ -371,10 +394,14 @@ __device__ __forceinline__ void compute_tile(TileRegs<FP8> &T, const QFrag<NB, Q
         const int w = mb >> 1;
         const uint32_t sel = (mb & 1) ? 0x07060302u : 0x05040100u;
         u32x4 a;
-        a.x = __builtin_amdgcn_perm(vb[1][w], vb[0][w], sel);
-        a.y = __builtin_amdgcn_perm(vb[3][w], vb[2][w], sel);
-        a.z = __builtin_amdgcn_perm(vb[5][w], vb[4][w], sel);
-        a.w = __builtin_amdgcn_perm(vb[7][w], vb[6][w], sel);
+        if constexpr (VTR) {
+            a = vb[mb];
+        } else {
+            a.x = __builtin_amdgcn_perm(vb[1][w], vb[0][w], sel);
+            a.y = __builtin_amdgcn_perm(vb[3][w], vb[2][w], sel);
+            a.z = __builtin_amdgcn_perm(vb[5][w], vb[4][w], sel);
+            a.w = __builtin_amdgcn_perm(vb[7][w], vb[6][w], sel);
+        }
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb) st.acc[mb][nb] = mfma_bf16(a, pb[nb], st.acc[mb][nb]);
     }
@@ -533,7 +560,7 @@ __device__ __forceinline__ void begin_rows(const Problem &p, int b, int h, int n
 // Write the rows of blocks rb0 .. rb0+NB-1: final output + lse when the worker
 // covered the whole segment, else a partial (normalised output, base-2 lse)
 // into workspace slot `slot`.
-template <bool FP8, int NB, bool LS>
+template <bool FP8, int NB, bool LS, bool VTR = false>
 __device__ __forceinline__ void end_rows(const Problem &p, const Plan &pl, SoftmaxState<NB, LS> &st,
                                          int b, int h, int rb0, bool whole, int64_t slot, int lane) {
     const int n16 = lane & 15, j = lane >> 4;
@@ -554,7 +581,24 @@ __device__ __forceinline__ void end_rows(const Problem &p, const Plan &pl, Softm
         // score was visible, and the row is NaN as the definition has it
         const float inv = l > 0.f ? vs / l : (l == 0.f ? 0.f : l);
         const float lse2 = l > 0.f ? st.msub[nb] + log2f(l) : (l == 0.f ? -INFINITY : l);
-        if (whole) {
+        if (VTR && whole) {  // lane holds dims 16 mb + 4j .. 16 mb + 4j + 3 of every block mb
+            const int64_t off = row_offset(p, b, h, r) + 4 * j;
+#pragma unroll
+            for (int mb = 0; mb < 8; ++mb) {
+                const f32x4 v = st.acc[mb][nb] * inv;
+                if (p.out_dtype == SPIRE_BF16)
+                    *reinterpret_cast<u32x2 *>(reinterpret_cast<uint16_t *>(p.out) + off + 16 * mb) =
+                        u32x2{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
+                else
+                    *reinterpret_cast<f32x4 *>(reinterpret_cast<float *>(p.out) + off + 16 * mb) = v;
+            }
+            if (j == 0 && p.lse != nullptr) p.lse[lse_index(p, b, h, r)] = lse2 * 0.69314718055994531f;
+        } else if (VTR) {
+            float *o = pl.part_o + (slot * pl.rows + r) * (int64_t)p.D + 4 * j;
+#pragma unroll
+            for (int mb = 0; mb < 8; ++mb) *reinterpret_cast<f32x4 *>(o + 16 * mb) = st.acc[mb][nb] * inv;
+            if (j == 0) pl.part_lse[slot * pl.rows + r] = lse2;
+        } else if (whole) {
             const int64_t off = row_offset(p, b, h, r) + 32 * j;
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
