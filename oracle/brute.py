@@ -39,8 +39,13 @@ def _attend(qrow, keys, vals, allowed):
             scores.append(sum(a * b for a, b in zip(qrow, keys[p])))
         else:
             scores.append(-math.inf)
-    M = max(scores) if scores else -math.inf
-    if M == -math.inf:
+    # a NaN score makes the maximum NaN (Python's max() would depend on where
+    # the NaN sits), and with it every weight: the row is NaN
+    if any(s != s for s in scores):
+        M = math.nan
+    else:
+        M = max(scores) if scores else -math.inf
+    if M == -math.inf:  # no visible key, or every visible score is -inf (weighs zero)
         return [0.0] * len(qrow), -math.inf
     w = [math.exp(s - M) for s in scores]
     L = sum(w)

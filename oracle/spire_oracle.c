@@ -27,7 +27,10 @@
  *  two-pass softmax:         M = max_j s_j,  w_j = exp(s_j - M),  L = sum w_j
  *  output:                   o_d = sum_j w_j * V_j,d / L,   lse = M + ln L
  *  Grouped-query attention:  query head h reads KV head h / (Hq / Hkv).
- *  A row with no visible key outputs zeros and lse = -inf.
+ *  A row with no visible key outputs zeros and lse = -inf.  A visible key whose
+ *  score is -inf weighs zero (exp(-inf) = 0), so a row whose visible scores are
+ *  all -inf is such an empty row too; a NaN score (a NaN key, or +inf met by
+ *  -inf in the dot product) or a score of +inf makes the row NaN.
  *
  * Storage decoding (own implementation):
  *   f32   as stored;
@@ -132,8 +135,9 @@ static void attend_row(const double *q, int D, double sm_scale,
         *lse = -INFINITY;
         return;
     }
-    /* pass 1: scores and their maximum */
+    /* pass 1: scores and their maximum (a NaN score is noted, not compared) */
     double M = -INFINITY;
+    int nan_score = 0;
     for (t = 0; t < nvis; ++t) {
         const oracle_kv *kv = views[src[t]];
         double ks = (kv->dtype == OR_FP8) ? (double)kv->k_scale[h] : 1.0;
@@ -141,7 +145,16 @@ static void attend_row(const double *q, int D, double sm_scale,
         for (d = 0; d < D; ++d)
             dot += q[d] * (load_elem(kv->k, kv->dtype, keys[t] + d) * ks);
         scores[t] = sm_scale * dot;
-        if (scores[t] > M) M = scores[t];
+        if (isnan(scores[t])) nan_score = 1;
+        else if (scores[t] > M) M = scores[t];
+    }
+    /* A score of -inf weighs zero, as a masked key does, so a row whose visible
+     * scores are all -inf is an empty row: zeros and lse = -inf.  A NaN score
+     * makes the whole row NaN (pass 2 below computes exactly that). */
+    if (M == -INFINITY && !nan_score) {
+        for (d = 0; d < D; ++d) out[d] = 0.0;
+        *lse = -INFINITY;
+        return;
     }
     /* pass 2: weights, normaliser and weighted sum of values */
     double L = 0.0;

@@ -37,11 +37,39 @@ MUTANTS = {
     "normaliser_dropped": ("for (d = 0; d < D; ++d) out[d] /= L;", "for (d = 0; d < D; ++d) out[d] /= 1.0;"),
     "value_head_wrong": ("double vs = (kv->dtype == OR_FP8) ? (double)kv->v_scale[h] : 1.0;",
                          "double vs = (kv->dtype == OR_FP8) ? (double)kv->v_scale[0] : 1.0;"),
+    "neg_inf_row_not_empty": ("if (M == -INFINITY && !nan_score) {", "if (0) {"),
+    "nan_score_not_noted": ("if (isnan(scores[t])) nan_score = 1;", "if (0) nan_score = 1;"),
 }
+
+
+def _nonfinite_case_ok(lib_path):
+    """Rows whose visible scores are all -inf (empty rows), partly -inf, and
+    -inf mixed with a NaN score (NaN rows), against the brute force."""
+    spec = W.VerifySpec(B=3, Hq=4, Hkv=2, D=8, k=2, ctx_lo=10, ctx_hi=10, kv_dtype="f32",
+                        q_dtype="f32", page_size=0, log_uniform=False)
+    inp = W.make_verify_inputs(spec, 29, keep_logical=True)
+    inp.q[..., 0] = -inp.q[..., 0].abs() - 0.5
+    n = int(inp.kv_lens[0])
+    for t in (inp.k_cache, inp.logical_k):
+        t[0, :, :n, 0] = float("inf")
+        t[1, :, :n - 2, 0] = float("inf")
+        t[2, :, :n, 0] = float("inf")
+        t[2, 0, 3, 1] = float("nan")
+    o, l = O.verify(inp.q, inp.k_cache, inp.v_cache, inp.kv_lens, 2, inp.sm_scale, lib_path=lib_path)
+    with np.errstate(invalid="ignore"):
+        bo, bl = brute.verify(inp.q, inp.logical_k, inp.logical_v, inp.kv_lens.tolist(), 2,
+                              inp.sm_scale)
+    if not (np.array_equal(np.isnan(o), np.isnan(bo)) and np.array_equal(np.isnan(l), np.isnan(bl))
+            and np.array_equal(np.isneginf(l), np.isneginf(bl))):
+        return False
+    fin, lfin = np.isfinite(bo), np.isfinite(bl)
+    return bool(np.max(np.abs(o[fin] - bo[fin])) <= 1e-12 and np.max(np.abs(l[lfin] - bl[lfin])) <= 1e-12)
 
 
 def _battery(lib_path):
     """Return True when the library agrees with every pin in the battery."""
+    if not _nonfinite_case_ok(lib_path):
+        return False
     for dtype in ("bf16", "fp8"):
         for ps in (0, 4):
             spec = W.VerifySpec(B=3, Hq=4, Hkv=2, D=8, k=3, ctx_lo=1, ctx_hi=30, kv_dtype=dtype,

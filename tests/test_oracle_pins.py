@@ -358,3 +358,81 @@ def test_nonfinite_visible_keys_match_brute_force(ps):
     assert np.array_equal(np.isfinite(o), fin) and np.array_equal(np.isfinite(l), lfin)
     assert np.max(np.abs(o[fin] - bo[fin])) <= TOL
     assert np.max(np.abs(l[lfin] - bl[lfin])) <= TOL
+
+
+@pytest.mark.parametrize("ps", [0, 4])
+def test_rows_with_all_visible_scores_neg_inf_are_empty_rows(ps):
+    """A score of -inf weighs zero, like a masked key, so a row whose visible
+    scores are all -inf is an empty row (zeros, lse -inf); one finite visible
+    key among -inf scores gives that key's value row and score exactly; -inf
+    scores mixed with a NaN score make the row NaN wherever the NaN sits.  The
+    C oracle against the brute force and against these closed forms."""
+    inp = vin(B=3, Hq=4, Hkv=2, D=8, k=2, lo=10, hi=10, dtype="f32", ps=ps, seed=23)
+    n = int(inp.kv_lens[0])          # every sequence holds n = 13 keys; k = 2
+    k = inp.spec.k
+    # every query has a negative first component, so K[.., 0] = +inf scores -inf
+    inp.q[..., 0] = -inp.q[..., 0].abs() - 0.5
+
+    def put(tensor_s, tensor_l, b, h, p, d, val):
+        tensor_l[b, h, p, d] = val
+        if ps:
+            page = int(inp.block_table[b, p // ps])
+            tensor_s[page, h, p % ps, d] = val
+        else:
+            tensor_s[b, h, p, d] = val
+    inf, nan = float("inf"), float("nan")
+    for h in range(2):                # sequence 0: every key of both heads scores -inf
+        for p in range(n):
+            put(inp.k_cache, inp.logical_k, 0, h, p, 0, inf)
+    for h in range(2):                # sequence 1: the keys query 0 sees score -inf
+        for p in range(n - k):
+            put(inp.k_cache, inp.logical_k, 1, h, p, 0, inf)
+    for p in range(n):                # sequence 2, head 0: -inf everywhere but a NaN key
+        put(inp.k_cache, inp.logical_k, 2, 0, p, 0, inf)
+    put(inp.k_cache, inp.logical_k, 2, 0, 0, 1, nan)        # first position ...
+    for p in range(n):                # ... head 1: the NaN key is the last one query 0 sees
+        put(inp.k_cache, inp.logical_k, 2, 1, p, 0, inf)
+    put(inp.k_cache, inp.logical_k, 2, 1, n - k - 1, 1, nan)
+    o, l = oracle_verify(inp)
+    with np.errstate(invalid="ignore"):
+        bo, bl = brute.verify(inp.q, inp.logical_k, inp.logical_v, inp.kv_lens.tolist(), k,
+                              inp.sm_scale)
+    # sequence 0: empty rows
+    assert np.all(o[0] == 0.0) and np.all(np.isneginf(l[0]))
+    # sequence 1: query 0 empty; query 1 sees exactly one finite key (position n-k)
+    assert np.all(o[1, 0] == 0.0) and np.all(np.isneginf(l[1, 0]))
+    V = inp.logical_v.double().numpy()
+    K = inp.logical_k.double().numpy()
+    Q = inp.q.double().numpy()
+    for h in range(4):
+        hk = h // 2
+        assert np.array_equal(o[1, 1, h], V[1, hk, n - k])
+        s = inp.sm_scale * float(np.dot(Q[1, 1, h], K[1, hk, n - k]))
+        assert abs(l[1, 1, h] - s) <= TOL
+    # sequence 2: the NaN key is visible to every row of both heads
+    assert np.all(np.isnan(o[2])) and np.all(np.isnan(l[2]))
+    # the brute force agrees element by element, pattern and value
+    assert np.array_equal(np.isnan(o), np.isnan(bo)) and np.array_equal(np.isnan(l), np.isnan(bl))
+    assert np.array_equal(np.isneginf(l), np.isneginf(bl))
+    fin, lfin = np.isfinite(bo), np.isfinite(bl)
+    assert np.array_equal(np.isfinite(o), fin) and np.array_equal(np.isfinite(l), lfin)
+    assert np.max(np.abs(o[fin] - bo[fin])) <= TOL
+    assert np.max(np.abs(l[lfin] - bl[lfin])) <= TOL
+
+
+def test_draft_row_with_all_visible_scores_neg_inf_is_empty():
+    """The same reading through the draft's sink + window mask."""
+    inp = din(B=2, Hq=4, Hkv=2, D=8, S=2, Wn=5, steps=1, lo=12, hi=12, dtype="f32", seed=24)
+    W.write_step_token(inp, 0)
+    inp.q[0][..., 0] = -inp.q[0][..., 0].abs() - 0.5
+    inp.sink_k[0, :, :, 0] = float("inf")       # sequence 0: sinks and every ring slot
+    inp.ring_k[0, :, :, 0] = float("inf")
+    inp.logical_k[0, :, :, 0] = float("inf")
+    o, l = oracle_draft(inp, 0)
+    bo, bl = brute.draft(inp.q[0], inp.logical_k, inp.logical_v, inp.seq_lens(0).tolist(),
+                         inp.spec.S, inp.spec.W, inp.sm_scale)
+    assert np.all(o[0] == 0.0) and np.all(np.isneginf(l[0]))
+    assert np.all(np.isfinite(o[1])) and np.all(np.isfinite(l[1]))
+    assert np.array_equal(np.isneginf(l), np.isneginf(bl))
+    assert np.max(np.abs(o - bo)) <= TOL
+    assert np.max(np.abs(l[1] - bl[1])) <= TOL
