@@ -39,6 +39,9 @@
  *    (fixed work partition, no floating-point atomics).
  *  - On a non-OK status spire_last_error() returns a message for the calling
  *    thread.
+ *  - The library holds no mutable state besides a per-device cache of the
+ *    compute-unit count: calls from several host threads, each with its own
+ *    workspace, need no locking.
  */
 #ifndef SPIRE_H
 #define SPIRE_H
@@ -124,10 +127,13 @@ size_t spire_verify_workspace_size(int32_t B, int32_t Hq, int32_t Hkv, int32_t D
  *   workspace >= spire_verify_workspace_size(B, Hq, Hkv, D, k) bytes of device
  *            memory, 256-byte aligned; its contents need no initialisation.
  * Supported storage: KV f32, bf16 or fp8 (fp8 needs k_scale and v_scale).
- * Non-finite values in the visible keys act as in the definition: a NaN key
- * or value, or a key whose score is +inf, makes the rows that see it NaN
- * (output and lse); a score of -inf weighs zero.  Storage outside the visible
- * keys never influences a result, whatever it holds.
+ * Non-finite values in the visible keys act as in the definition: a NaN key,
+ * or a key whose score is +inf, makes the rows that see it NaN (output and
+ * lse); a NaN or infinite value makes the output elements of its dimension
+ * NaN or infinite in the rows that see it; a score of -inf weighs zero, so a
+ * row whose visible scores are all -inf is an empty row.  Storage outside a
+ * row's visible keys never influences that row, whatever it holds -- also
+ * keys [n_b - k + i, n_b), which only later rows see.
  */
 spire_status spire_verify_attn(const void *q, int32_t q_dtype, const spire_kv *kv,
                                const int32_t *kv_lens, int32_t B, int32_t Hq, int32_t Hkv,
@@ -298,8 +304,7 @@ spire_status spire_feedback_memory(const void *x, int32_t x_dtype, const float *
  *   buf   16-byte aligned, bytes a multiple of 16 (0 is allowed: nothing read,
  *         the sink still written);
  *   sink  4-byte aligned.
- * Asynchronous on `stream`; allocates nothing.  Kernel id 10 in the timing
- * records.
+ * Asynchronous on `stream`; allocates nothing.
  */
 #define SPIRE_HBM_PROBE_SINK_WORDS 2048
 spire_status spire_hbm_read_probe(const void *buf, size_t bytes, uint32_t *sink, size_t sink_words,
@@ -316,32 +321,64 @@ const char *spire_last_error(void);
 int32_t spire_version(void);
 
 /*
- * Kernel selection, process-wide: 0 = automatic (matrix-core kernels where the
- * dtype and shape allow -- LDS-staged for more than 32 rows per KV head,
- * register-staged otherwise -- and the generic vector kernel for the
- * rest), 1 = always the generic vector kernel, 2 = prefer the register-staged
- * matrix-core kernel (it holds at most 32 rows), 3 = prefer the LDS-staged one
- * (it takes bf16 K/V only above 32 rows), each where its limits allow.
- * Returns SPIRE_ERR_INVALID_ARG for other values.
+ * Per-call options of the entry points that launch several kernels
+ * (spire_verify_attn_ex, spire_draft_sparse_attn_ex, spire_token_verify_ex).
+ * A NULL pointer, or a zero-initialised struct, means the defaults; the
+ * library reads the struct and writes the host arrays it points to only
+ * during the call and keeps nothing afterwards, so calls stay reentrant.
+ *   kernel        attention family (the token entry point ignores it):
+ *                 0 automatic -- the matrix-core kernels where dtype and shape
+ *                 allow (LDS-staged above 32 rows per KV head, register-staged
+ *                 otherwise), the generic vector kernel for the rest;
+ *                 1 always the generic vector kernel; 2 prefer the
+ *                 register-staged kernel (at most 32 rows); 3 prefer the
+ *                 LDS-staged one (bf16 K/V only above 32 rows); each where its
+ *                 limits allow.  Results agree within the stated tolerances;
+ *                 the choice exists for measurement and cross-checks.
+ *   max_launches  capacity of the two arrays below; 0 records nothing.
+ *   events        host array [2 * max_launches] of events the CALLER created
+ *                 (hipEventCreate, timing enabled) on the stream's device:
+ *                 events[2i] is recorded on `stream` right before the i-th
+ *                 kernel the call launches, events[2i + 1] right after it.
+ *                 Launches beyond max_launches are not recorded.
+ *   kernel_ids    host array [max_launches] or NULL: the id of each recorded
+ *                 launch -- 0 plan, 1 verify partial attention, 2 draft
+ *                 partial attention, 3 combine, 4 token verification weights,
+ *                 5 token verification select, 11 the check of the values of
+ *                 keys [n - k, n) after a matrix-core verify call.
+ *   n_launches    host int32 or NULL: set to the number of kernels the call
+ *                 launched (0 when it returned before launching).
+ *   reserved      must be 0.
+ * Invalid options return SPIRE_ERR_INVALID_ARG before anything is enqueued.
  */
-spire_status spire_set_kernel_variant(int32_t variant);
+typedef struct spire_launch_opts {
+    int32_t kernel;
+    int32_t max_launches;
+    hipEvent_t *events;
+    int32_t *kernel_ids;
+    int32_t *n_launches;
+    int32_t reserved;
+} spire_launch_opts;
 
-/*
- * Per-kernel timing for measurement.  spire_timing_enable(1) creates HIP
- * events (this allocates; call it outside timed regions) and from then on
- * every entry point records an event pair around each kernel it launches, on
- * the caller's stream.  spire_timing_collect waits for the recorded events,
- * writes up to `max` (kernel id, milliseconds) pairs in launch order and
- * returns how many it wrote, then forgets them.  Kernel ids: 0 plan,
- * 1 verify partial attention, 2 draft partial attention, 3 combine,
- * 4 token verification weights, 5 token verification select, 6 kv append,
- * 7 draft append, 8 draft rollback, 9 feedback memory, 10 streaming-read
- * probe.  At most
- * 4096 launches are kept between collects (older ones are dropped).
- * spire_timing_enable(0) releases the events.  Not thread-safe.
- */
-spire_status spire_timing_enable(int32_t on);
-int32_t spire_timing_collect(int32_t *kernel_ids, float *ms, int32_t max);
+spire_status spire_verify_attn_ex(const void *q, int32_t q_dtype, const spire_kv *kv,
+                                  const int32_t *kv_lens, int32_t B, int32_t Hq, int32_t Hkv,
+                                  int32_t D, int32_t k, float sm_scale, void *out,
+                                  int32_t out_dtype, float *lse, void *workspace,
+                                  size_t workspace_bytes, hipStream_t stream,
+                                  const spire_launch_opts *opts);
+spire_status spire_draft_sparse_attn_ex(const void *q, int32_t q_dtype, const spire_kv *sink,
+                                        const spire_kv *ring, const int32_t *seq_lens,
+                                        const int32_t *ring_offset, int32_t B, int32_t Hq,
+                                        int32_t Hkv, int32_t D, int32_t S, int32_t W, float sm_scale,
+                                        void *out, int32_t out_dtype, float *lse, void *workspace,
+                                        size_t workspace_bytes, hipStream_t stream,
+                                        const spire_launch_opts *opts);
+spire_status spire_token_verify_ex(const float *p_target, const float *q_draft,
+                                   const int32_t *draft_tokens, const float *u_accept,
+                                   const float *u_sample, int32_t B, int32_t k, int32_t V,
+                                   int32_t *n_accepted, int32_t *out_tokens, void *workspace,
+                                   size_t workspace_bytes, hipStream_t stream,
+                                   const spire_launch_opts *opts);
 
 #ifdef __cplusplus
 }

@@ -131,14 +131,16 @@ def verify(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor, kv_len
 
 def draft(q: torch.Tensor, sink_k, sink_v, ring_k, ring_v, seq_lens, ring_offset, S: int, W: int,
           sm_scale: float, k_scale=None, v_scale=None, seq_ids: Optional[Sequence[int]] = None,
-          lib_path: Optional[str] = None):
+          lib_path: Optional[str] = None, sink_k_scale=None, sink_v_scale=None):
     """fp64 draft sparse attention for one step.  q [B, Hq, D]; sink [B, Hkv, S, D];
-    ring [B, Hkv, W, D].  Returns (out [nsel, Hq, D], lse [nsel, Hq])."""
+    ring [B, Hkv, W, D]; fp8 scales per view (the sink's default to the ring's).
+    Returns (out [nsel, Hq, D], lse [nsel, Hq])."""
     keep = []
     B, Hq, D = q.shape
     Hkv = ring_k.shape[1] if W > 0 else sink_k.shape[1]
     dt = _dtype_name(ring_k if W > 0 else sink_k)
-    sink = _kv_struct(sink_k, sink_v, 0, None, k_scale, v_scale, dt, keep)
+    sink = _kv_struct(sink_k, sink_v, 0, None, k_scale if sink_k_scale is None else sink_k_scale,
+                      v_scale if sink_v_scale is None else sink_v_scale, dt, keep)
     ring = _kv_struct(ring_k, ring_v, 0, None, k_scale, v_scale, dt, keep)
     qh = _host(q)
     lens = _host(torch.as_tensor(seq_lens).to(torch.int32))

@@ -90,6 +90,113 @@ __device__ __forceinline__ float wave_sum(float x) {
     return x;
 }
 
+// One 16-row unit (rows r0 .. r0+15 of KV head h of sequence b, of n keys)
+// over tiles [t0, t1): queries in qs, probabilities through ps.  Writes the
+// final rows when `whole`, else a partial into workspace slot `slot`.  A value
+// is only accumulated for the rows that see its key, so that a non-finite
+// value of a key some rows mask reaches only the rows that see it.
+__device__ __forceinline__ void generic_unit(const Problem &p, const Plan &pl, int b, int h, int r0, int n,
+                                             int ns, int rs, int t0, int t1, bool whole, int64_t slot, int lane,
+                                             float (*qs)[kMaxD], float (*ps)[KT]) {
+    const int D = p.D;
+    __syncthreads();  // previous unit finished reading qs / ps
+    for (int idx = lane; idx < RB * D; idx += 64) {
+        const int r = idx / D, d = idx - (idx / D) * D;
+        float v = 0.f;
+        if (r0 + r < p.R) {
+            const int64_t off = row_offset(p, b, h, r0 + r) + d;
+            v = p.q_dtype == SPIRE_F32 ? reinterpret_cast<const float *>(p.q)[off]
+                                       : bf16_to_f32(reinterpret_cast<const uint16_t *>(p.q)[off]);
+        }
+        qs[r][d] = v;
+    }
+    __syncthreads();
+
+    float m[RB], l[RB], acc[RB][2];
+    int lim[RB];
+#pragma unroll
+    for (int r = 0; r < RB; ++r) {
+        m[r] = -INFINITY; l[r] = 0.f; acc[r][0] = 0.f; acc[r][1] = 0.f;
+        lim[r] = (r0 + r < p.R) ? visible_limit(p, n, r0 + r) : n;
+    }
+
+    for (int t = t0; t < t1 && n > 0; ++t) {
+        const int kb = t * KT;
+        const int key = kb + lane;
+        const int kc = key < n ? key : n - 1;
+        const RowRef rr = key_row(p, b, h, kc, ns, rs);
+        float s[RB];
+#pragma unroll
+        for (int r = 0; r < RB; ++r) s[r] = 0.f;
+        for (int d = 0; d < D; ++d) {
+            const float kx = load_elem(rr.k, d, p.kv_dtype);
+#pragma unroll
+            for (int r = 0; r < RB; ++r) s[r] += kx * qs[r][d];
+        }
+        const float sc = p.sm_scale_log2 * rr.ks;
+#pragma unroll
+        for (int r = 0; r < RB; ++r) {
+            float x = key < lim[r] ? s[r] * sc : -INFINITY;
+            const float mnew = fmaxf(m[r], wave_max(x));
+            const float msub = mnew == -INFINITY ? 0.f : mnew;
+            const float alpha = exp2f(m[r] - msub);
+            const float pr = exp2f(x - msub);
+            m[r] = mnew;
+            l[r] = l[r] * alpha + pr;
+            acc[r][0] *= alpha;
+            acc[r][1] *= alpha;
+            ps[r][lane] = pr;
+        }
+        __syncthreads();
+        const int nv = n - kb < KT ? n - kb : KT;
+        for (int tk = 0; tk < nv; ++tk) {
+            const RowRef vr = key_row(p, b, h, kb + tk, ns, rs);
+            const float v0 = load_elem(vr.v, lane, p.kv_dtype) * vr.vs;
+            const float v1 = lane + 64 < D ? load_elem(vr.v, lane + 64, p.kv_dtype) * vr.vs : 0.f;
+#pragma unroll
+            for (int r = 0; r < RB; ++r) {
+                if (kb + tk >= lim[r]) continue;  // uniform: masked for this row (0 * inf would be NaN)
+                const float pr = ps[r][tk];
+                acc[r][0] += pr * v0;
+                acc[r][1] += pr * v1;
+            }
+        }
+        __syncthreads();
+    }
+
+#pragma unroll
+    for (int r = 0; r < RB; ++r) {
+        const float L = wave_sum(l[r]);
+        if (r0 + r >= p.R) continue;
+        // L == 0: no visible key; L NaN: a NaN key or a +inf score was visible
+        const float inv = L > 0.f ? 1.f / L : (L == 0.f ? 0.f : L);
+        const float lse2 = L > 0.f ? m[r] + log2f(L) : (L == 0.f ? -INFINITY : L);
+        if (whole) {
+            const int64_t off = row_offset(p, b, h, r0 + r);
+#pragma unroll
+            for (int dd = 0; dd < 2; ++dd) {
+                const int d = lane + 64 * dd;
+                if (d >= D) continue;
+                const float o = acc[r][dd] * inv;
+                if (p.out_dtype == SPIRE_BF16)
+                    reinterpret_cast<uint16_t *>(p.out)[off + d] = f32_to_bf16_rne(o);
+                else
+                    reinterpret_cast<float *>(p.out)[off + d] = o;
+            }
+            if (lane == 0 && p.lse != nullptr)
+                p.lse[lse_index(p, b, h, r0 + r)] = lse2 * 0.69314718055994531f;
+        } else {
+            float *o = pl.part_o + (slot * pl.rows + r) * (int64_t)D;
+#pragma unroll
+            for (int dd = 0; dd < 2; ++dd) {
+                const int d = lane + 64 * dd;
+                if (d < D) o[d] = acc[r][dd] * inv;
+            }
+            if (lane == 0) pl.part_lse[slot * pl.rows + r] = lse2;
+        }
+    }
+}
+
 __global__ __launch_bounds__(64) void generic_partial_kernel(Problem p, Plan pl) {
     __shared__ float qs[RB][kMaxD];
     __shared__ float ps[RB][KT];
@@ -104,7 +211,6 @@ __global__ __launch_bounds__(64) void generic_partial_kernel(Problem p, Plan pl)
     int seg = pl.wstart[2 * wid];
     int tile = pl.wstart[2 * wid + 1];
     const int nrb = pl.units / p.Hkv;
-    const int D = p.D;
 
     while (pos < end) {
         const int b = seg / pl.units;
@@ -135,108 +241,58 @@ __global__ __launch_bounds__(64) void generic_partial_kernel(Problem p, Plan pl)
                 rs = (n - ns == p.W) ? 0 : (o + first % p.W) % p.W;
             }
         }
-
-        __syncthreads();  // previous segment finished reading qs / ps
-        for (int idx = lane; idx < RB * D; idx += 64) {
-            const int r = idx / D, d = idx - (idx / D) * D;
-            float v = 0.f;
-            if (r0 + r < p.R) {
-                const int64_t off = row_offset(p, b, h, r0 + r) + d;
-                v = p.q_dtype == SPIRE_F32 ? reinterpret_cast<const float *>(p.q)[off]
-                                           : bf16_to_f32(reinterpret_cast<const uint16_t *>(p.q)[off]);
-            }
-            qs[r][d] = v;
-        }
-        __syncthreads();
-
-        float m[RB], l[RB], acc[RB][2];
-        int lim[RB];
-#pragma unroll
-        for (int r = 0; r < RB; ++r) {
-            m[r] = -INFINITY; l[r] = 0.f; acc[r][0] = 0.f; acc[r][1] = 0.f;
-            lim[r] = (r0 + r < p.R) ? visible_limit(p, n, r0 + r) : n;
-        }
-
-        for (int t = tile; t < t1 && n > 0; ++t) {
-            const int kb = t * KT;
-            const int key = kb + lane;
-            const int kc = key < n ? key : n - 1;
-            const RowRef rr = key_row(p, b, h, kc, ns, rs);
-            float s[RB];
-#pragma unroll
-            for (int r = 0; r < RB; ++r) s[r] = 0.f;
-            for (int d = 0; d < D; ++d) {
-                const float kx = load_elem(rr.k, d, p.kv_dtype);
-#pragma unroll
-                for (int r = 0; r < RB; ++r) s[r] += kx * qs[r][d];
-            }
-            const float sc = p.sm_scale_log2 * rr.ks;
-#pragma unroll
-            for (int r = 0; r < RB; ++r) {
-                float x = key < lim[r] ? s[r] * sc : -INFINITY;
-                const float mnew = fmaxf(m[r], wave_max(x));
-                const float msub = mnew == -INFINITY ? 0.f : mnew;
-                const float alpha = exp2f(m[r] - msub);
-                const float pr = exp2f(x - msub);
-                m[r] = mnew;
-                l[r] = l[r] * alpha + pr;
-                acc[r][0] *= alpha;
-                acc[r][1] *= alpha;
-                ps[r][lane] = pr;
-            }
-            __syncthreads();
-            const int nv = n - kb < KT ? n - kb : KT;
-            for (int tk = 0; tk < nv; ++tk) {
-                const RowRef vr = key_row(p, b, h, kb + tk, ns, rs);
-                const float v0 = load_elem(vr.v, lane, p.kv_dtype) * vr.vs;
-                const float v1 = lane + 64 < D ? load_elem(vr.v, lane + 64, p.kv_dtype) * vr.vs : 0.f;
-#pragma unroll
-                for (int r = 0; r < RB; ++r) {
-                    const float pr = ps[r][tk];
-                    acc[r][0] += pr * v0;
-                    acc[r][1] += pr * v1;
-                }
-            }
-            __syncthreads();
-        }
-
         const bool whole = (tile == 0 && t1 == tiles_b);
         const int64_t slot = 2 * (int64_t)wid + (pos == begin ? 0 : 1);
-#pragma unroll
-        for (int r = 0; r < RB; ++r) {
-            const float L = wave_sum(l[r]);
-            if (r0 + r >= p.R) continue;
-            // L == 0: no visible key; L NaN: a NaN key or a +inf score was visible
-            const float inv = L > 0.f ? 1.f / L : (L == 0.f ? 0.f : L);
-            const float lse2 = L > 0.f ? m[r] + log2f(L) : (L == 0.f ? -INFINITY : L);
-            if (whole) {
-                const int64_t off = row_offset(p, b, h, r0 + r);
-#pragma unroll
-                for (int dd = 0; dd < 2; ++dd) {
-                    const int d = lane + 64 * dd;
-                    if (d >= D) continue;
-                    const float o = acc[r][dd] * inv;
-                    if (p.out_dtype == SPIRE_BF16)
-                        reinterpret_cast<uint16_t *>(p.out)[off + d] = f32_to_bf16_rne(o);
-                    else
-                        reinterpret_cast<float *>(p.out)[off + d] = o;
-                }
-                if (lane == 0 && p.lse != nullptr)
-                    p.lse[lse_index(p, b, h, r0 + r)] = lse2 * 0.69314718055994531f;
-            } else {
-                float *o = pl.part_o + (slot * pl.rows + r) * (int64_t)D;
-#pragma unroll
-                for (int dd = 0; dd < 2; ++dd) {
-                    const int d = lane + 64 * dd;
-                    if (d < D) o[d] = acc[r][dd] * inv;
-                }
-                if (lane == 0) pl.part_lse[slot * pl.rows + r] = lse2;
-            }
-        }
+        generic_unit(p, pl, b, h, r0, n, ns, rs, tile, t1, whole, slot, lane, qs, ps);
         pos += te - tile;
         ++seg;
         tile = 0;
     }
+}
+
+// ---- non-finite values among the keys only some rows see ------------------------
+// Keys [n - k, n) of a verify segment are visible to the later draft rows only.
+// In the matrix-core kernels the rows that mask such a key still multiply its
+// value by a zero probability, and 0 * inf or 0 * NaN is NaN: a non-finite
+// value there (e.g. fp8 0x7F written for a NaN) would reach rows that must not
+// see it.  This pass, launched after the combine of a matrix-core verify call,
+// checks those few value rows of every (sequence, KV head); a segment holding a
+// non-finite one (rare) has all its rows recomputed here by the fp32 unit loop
+// above, which only accumulates a value for the rows that see its key, and
+// overwritten.  Its cost otherwise is reading k value rows per segment.
+__device__ __forceinline__ bool word_nonfinite(uint32_t x, int dtype) {
+    if (dtype == SPIRE_F32) return (x & 0x7F800000u) == 0x7F800000u;
+    if (dtype == SPIRE_BF16) return (x & 0x7F80u) == 0x7F80u || (x & 0x7F800000u) == 0x7F800000u;
+    // e4m3fn: NaN is S.1111.111 (no infinities)
+    return (x & 0x7Fu) == 0x7Fu || ((x >> 8) & 0x7Fu) == 0x7Fu || ((x >> 16) & 0x7Fu) == 0x7Fu ||
+           ((x >> 24) & 0x7Fu) == 0x7Fu;
+}
+
+__global__ __launch_bounds__(64) void tail_fix_kernel(Problem p, Plan pl) {
+    __shared__ float qs[RB][kMaxD];
+    __shared__ float ps[RB][KT];
+    const int lane = threadIdx.x;
+    const int b = blockIdx.x / p.Hkv, h = blockIdx.x - (blockIdx.x / p.Hkv) * p.Hkv;
+    const int n = effective_keys(p, b);
+    const int lo = n - p.k > 0 ? n - p.k : 0;
+    if (lo >= n) return;
+    // the value rows of keys [lo, n), as 4-byte words (row bytes are a multiple of 16)
+    const int words = p.D * p.kv.elem / 4;
+    bool bad = false;
+    for (int idx = lane; idx < (n - lo) * words; idx += 64) {
+        const int key = lo + idx / words, w = idx - (idx / words) * words;
+        const RowRef vr = key_row(p, b, h, key, 0, 0);
+        bad |= word_nonfinite(reinterpret_cast<const uint32_t *>(vr.v)[w], p.kv_dtype);
+    }
+    if (!__any(bad)) return;
+    const int tiles = (n + KT - 1) / KT;
+    for (int r0 = 0; r0 < p.R; r0 += RB) generic_unit(p, pl, b, h, r0, n, 0, 0, 0, tiles, true, 0, lane, qs, ps);
+}
+
+hipError_t launch_tail_fix(const Problem &p, const Plan &pl, hipStream_t st) {
+    if (p.draft || p.k == 0 || (int64_t)p.B * p.Hkv == 0) return hipSuccess;
+    hipLaunchKernelGGL(tail_fix_kernel, dim3((unsigned)(p.B * p.Hkv)), dim3(64), 0, st, p, pl);
+    return hipGetLastError();
 }
 
 hipError_t launch_generic_partial(const Problem &p, const Plan &pl, hipStream_t st) {

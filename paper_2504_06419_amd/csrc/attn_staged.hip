@@ -6,8 +6,9 @@
 //   * deep pipelines: a ring of NS tile stages per worker keeps NS-1 tiles in
 //     flight (fp8 tiles are only 8 KB, so register staging cannot hold
 //     enough bytes in flight to cover HBM latency);
-//   * room for many query rows: a bf16 worker, or an fp8 one with 3-4 row
-//     blocks, is P = 2 waves of one workgroup that share the stage ring and
+//   * room for many query rows: a bf16 worker, or an fp8 one with 3-4 or 6-8
+//     row blocks (up to 128 rows, e.g. k = 15 with 8 query heads per KV
+//     head), is P = 2 waves of one workgroup that share the stage ring and
 //     split the 16-row blocks between them, each keeping its accumulators in
 //     registers without spilling.  An fp8 worker with 5 blocks (the 72 rows of
 //     k = 8 with 8 query heads per KV head) is one wave with every block: it
@@ -276,6 +277,9 @@ static hipError_t launch_staged_fp(const Problem &p, const Plan &pl, int nb, hip
     case 3: return launch_staged_nb<FP8, 3, staged_waves(FP8, 3)>(p, pl, st);
     case 4: return launch_staged_nb<FP8, 4, staged_waves(FP8, 4)>(p, pl, st);
     case 5: return launch_staged_nb<FP8, 5, staged_waves(FP8, 5)>(p, pl, st);
+    case 6: return launch_staged_nb<FP8, 6, staged_waves(FP8, 6)>(p, pl, st);
+    case 7: return launch_staged_nb<FP8, 7, staged_waves(FP8, 7)>(p, pl, st);
+    case 8: return launch_staged_nb<FP8, 8, staged_waves(FP8, 8)>(p, pl, st);
     default: return hipErrorInvalidValue;
     }
 }

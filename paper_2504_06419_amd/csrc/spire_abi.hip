@@ -20,7 +20,6 @@ using namespace spire;
 namespace {
 
 thread_local char g_err[512] = "";
-int g_variant = 0;
 
 spire_status fail(spire_status s, const char *fmt, ...) {
     va_list ap;
@@ -88,36 +87,46 @@ size_t workspace_bytes_for(int B, int R, int D) {
     return a.total > b.total ? a.total : b.total;
 }
 
-// ---- timing -----------------------------------------------------------------
-constexpr int kTimingSlots = 4096;
-struct TimingRec {
-    hipEvent_t a, b;
-    int id;
+// ---- per-call options: kernel family and launch events ----------------------------
+// Kernel ids of the recorded launches (include/spire.h).
+enum { KID_PLAN = 0, KID_VERIFY = 1, KID_DRAFT = 2, KID_COMBINE = 3, KID_TOKEN_WEIGHTS = 4,
+       KID_TOKEN_SELECT = 5, KID_TAIL_CHECK = 11 };
+
+// Records the caller's events around each launch of one call, in launch order.
+struct Recorder {
+    const spire_launch_opts *o;
+    int n = 0;
+    explicit Recorder(const spire_launch_opts *opts) : o(opts) {}
+    template <class F>
+    hipError_t run(int id, hipStream_t st, F &&launch) {
+        const bool rec = o != nullptr && o->events != nullptr && n < o->max_launches;
+        hipError_t e = hipSuccess;
+        if (rec && (e = hipEventRecord(o->events[2 * n], st)) != hipSuccess) return e;
+        if ((e = launch()) != hipSuccess) return e;
+        if (rec) {
+            if ((e = hipEventRecord(o->events[2 * n + 1], st)) != hipSuccess) return e;
+            if (o->kernel_ids != nullptr) o->kernel_ids[n] = id;
+        }
+        ++n;
+        return hipSuccess;
+    }
+    hipError_t run(int id, hipStream_t st, hipError_t (*fn)(const Problem &, const Plan &, hipStream_t),
+                   const Problem &p, const Plan &pl) {
+        return run(id, st, [&] { return fn(p, pl, st); });
+    }
+    ~Recorder() {
+        if (o != nullptr && o->n_launches != nullptr) *o->n_launches = n;
+    }
 };
-std::vector<TimingRec> g_ev;
-int g_ev_next = 0, g_ev_count = 0;
-bool g_timing = false;
 
-// Record an event pair around one launch (a callable returning hipError_t)
-// on its stream while timing is enabled.
-template <class F>
-hipError_t timed_call(int id, hipStream_t st, F &&launch) {
-    if (!g_timing) return launch();
-    TimingRec &r = g_ev[g_ev_next];
-    r.id = id;
-    hipError_t e = hipEventRecord(r.a, st);
-    if (e != hipSuccess) return e;
-    e = launch();
-    if (e != hipSuccess) return e;
-    e = hipEventRecord(r.b, st);
-    g_ev_next = (g_ev_next + 1) % kTimingSlots;
-    if (g_ev_count < kTimingSlots) ++g_ev_count;
-    return e;
-}
-
-hipError_t timed_launch(int id, hipStream_t st, hipError_t (*fn)(const Problem &, const Plan &, hipStream_t),
-                        const Problem &p, const Plan &pl) {
-    return timed_call(id, st, [&] { return fn(p, pl, st); });
+spire_status check_opts(const spire_launch_opts *o) {
+    if (o == nullptr) return SPIRE_OK;
+    if (o->kernel < 0 || o->kernel > 3) return fail(SPIRE_ERR_INVALID_ARG, "opts->kernel must be 0..3 (got %d)", o->kernel);
+    if (o->max_launches < 0) return fail(SPIRE_ERR_INVALID_ARG, "opts->max_launches must be >= 0");
+    if (o->max_launches > 0 && o->events == nullptr)
+        return fail(SPIRE_ERR_INVALID_ARG, "opts->events is NULL with max_launches > 0");
+    if (o->reserved != 0) return fail(SPIRE_ERR_INVALID_ARG, "opts->reserved must be 0");
+    return SPIRE_OK;
 }
 
 // ---- argument checks --------------------------------------------------------
@@ -203,21 +212,23 @@ spire_status common_checks(const void *q, int q_dtype, int B, int Hq, int Hkv, i
 
 // Kernel family for a matrix-core eligible request: LDS-staged for more than
 // 32 rows (deep stage ring; the row blocks on two waves, or all five fp8
-// blocks on one), register-staged otherwise; the variant setting can force
-// either.
-bool use_staged(const Problem &p) {
+// blocks of 72-80 rows on one; up to 8 blocks, 128 rows), register-staged
+// otherwise; the caller's kernel choice can ask for the LDS-staged one.
+bool use_staged(const Problem &p, int kernel) {
     const int nb = (p.R + 15) / 16;
     if (nb > 2) return true;  // the register-staged kernel holds at most 32 rows
-    if (g_variant == 3) return p.kv_dtype == SPIRE_FP8_E4M3FN;
+    if (kernel == 3) return p.kv_dtype == SPIRE_FP8_E4M3FN;
     return false;  // measured: up to 32 rows the register-staged kernel is faster
 }
 
 spire_status run(Problem &p, bool use_mfma, void *workspace, size_t ws_bytes, hipStream_t stream,
-                 int partial_id) {
+                 int partial_id, const spire_launch_opts *opts) {
     int cus = 0;
     if (device_cus(&cus) != 0) return fail(SPIRE_ERR_HIP, "cannot query the current HIP device");
-    const bool mf = use_mfma && g_variant != 1;
-    const bool staged = mf && use_staged(p);
+    const int kernel = opts != nullptr ? opts->kernel : 0;
+    Recorder rec(opts);
+    const bool mf = use_mfma && kernel != 1;
+    const bool staged = mf && use_staged(p, kernel);
     const int nb = (p.R + 15) / 16;
     Plan pl;
     pl.tile = mf ? kMfmaTile : kGenericTile;
@@ -251,25 +262,31 @@ spire_status run(Problem &p, bool use_mfma, void *workspace, size_t ws_bytes, hi
     // read it from the plan kernel's output
     hipError_t e = hipSuccess;
     if (!mf || staged) {
-        e = timed_launch(0, stream, launch_plan, p, pl);
+        e = rec.run(KID_PLAN, stream, launch_plan, p, pl);
         if (e != hipSuccess) return fail(SPIRE_ERR_HIP, "plan launch: %s", hipGetErrorString(e));
     }
     if (staged) {
         auto fn = [](const Problem &pp, const Plan &pp2, hipStream_t s) {
             return launch_staged_partial(pp, pp2, (pp.R + 15) / 16, s);
         };
-        e = timed_launch(partial_id, stream, fn, p, pl);
+        e = rec.run(partial_id, stream, fn, p, pl);
     } else if (mf) {
         auto fn = [](const Problem &pp, const Plan &pp2, hipStream_t s) {
             return launch_mfma_partial(pp, pp2, (pp.R + 15) / 16, s);
         };
-        e = timed_launch(partial_id, stream, fn, p, pl);
+        e = rec.run(partial_id, stream, fn, p, pl);
     } else {
-        e = timed_launch(partial_id, stream, launch_generic_partial, p, pl);
+        e = rec.run(partial_id, stream, launch_generic_partial, p, pl);
     }
     if (e != hipSuccess) return fail(SPIRE_ERR_HIP, "attention launch: %s", hipGetErrorString(e));
-    e = timed_launch(3, stream, launch_combine, p, pl);
+    e = rec.run(KID_COMBINE, stream, launch_combine, p, pl);
     if (e != hipSuccess) return fail(SPIRE_ERR_HIP, "combine launch: %s", hipGetErrorString(e));
+    // the matrix-core kernels multiply the values of keys a row masks by zero:
+    // segments with a non-finite value among keys [n - k, n) are redone exactly
+    if (mf && !p.draft && p.k > 0) {
+        e = rec.run(KID_TAIL_CHECK, stream, launch_tail_fix, p, pl);
+        if (e != hipSuccess) return fail(SPIRE_ERR_HIP, "tail check launch: %s", hipGetErrorString(e));
+    }
     return SPIRE_OK;
 }
 
@@ -291,12 +308,6 @@ const char *spire_status_string(spire_status s) {
 }
 
 const char *spire_last_error(void) { return g_err; }
-
-spire_status spire_set_kernel_variant(int32_t variant) {
-    if (variant < 0 || variant > 3) return fail(SPIRE_ERR_INVALID_ARG, "variant must be 0..3");
-    g_variant = variant;
-    return SPIRE_OK;
-}
 
 size_t spire_verify_workspace_size(int32_t B, int32_t Hq, int32_t Hkv, int32_t D, int32_t k) {
     if (B < 0 || Hkv <= 0 || Hq <= 0 || Hq % Hkv != 0 || D <= 0 || k < 0) return 0;
@@ -320,8 +331,21 @@ spire_status spire_verify_attn(const void *q, int32_t q_dtype, const spire_kv *k
                                int32_t D, int32_t k, float sm_scale, void *out,
                                int32_t out_dtype, float *lse, void *workspace,
                                size_t workspace_bytes, hipStream_t stream) {
+    return spire_verify_attn_ex(q, q_dtype, kv, kv_lens, B, Hq, Hkv, D, k, sm_scale, out, out_dtype, lse,
+                                workspace, workspace_bytes, stream, nullptr);
+}
+
+spire_status spire_verify_attn_ex(const void *q, int32_t q_dtype, const spire_kv *kv,
+                                  const int32_t *kv_lens, int32_t B, int32_t Hq, int32_t Hkv,
+                                  int32_t D, int32_t k, float sm_scale, void *out,
+                                  int32_t out_dtype, float *lse, void *workspace,
+                                  size_t workspace_bytes, hipStream_t stream,
+                                  const spire_launch_opts *opts) {
     g_err[0] = '\0';
-    spire_status s = common_checks(q, q_dtype, B, Hq, Hkv, D, k, out, out_dtype, workspace);
+    if (opts != nullptr && opts->n_launches != nullptr) *opts->n_launches = 0;
+    spire_status s = check_opts(opts);
+    if (s != SPIRE_OK) return s;
+    s = common_checks(q, q_dtype, B, Hq, Hkv, D, k, out, out_dtype, workspace);
     if (s != SPIRE_OK) return s;
     s = check_scale(sm_scale);
     if (s != SPIRE_OK) return s;
@@ -357,8 +381,8 @@ spire_status spire_verify_attn(const void *q, int32_t q_dtype, const spire_kv *k
                (uint64_t)kv->page_size * kv->s_tok * es < (1ull << 31))
             : (kv->capacity >= 1);
     const bool mfma = (kv->dtype == SPIRE_BF16 || kv->dtype == SPIRE_FP8_E4M3FN) &&
-                      q_dtype == SPIRE_BF16 && D == 128 && p.R <= 80 && layout_ok && rows_aligned(kv);
-    return run(p, mfma, workspace, workspace_bytes, stream, 1);
+                      q_dtype == SPIRE_BF16 && D == 128 && p.R <= kMaxRows && layout_ok && rows_aligned(kv);
+    return run(p, mfma, workspace, workspace_bytes, stream, KID_VERIFY, opts);
 }
 
 spire_status spire_draft_sparse_attn(const void *q, int32_t q_dtype, const spire_kv *sink,
@@ -367,8 +391,22 @@ spire_status spire_draft_sparse_attn(const void *q, int32_t q_dtype, const spire
                                      int32_t Hkv, int32_t D, int32_t S, int32_t W, float sm_scale,
                                      void *out, int32_t out_dtype, float *lse, void *workspace,
                                      size_t workspace_bytes, hipStream_t stream) {
+    return spire_draft_sparse_attn_ex(q, q_dtype, sink, ring, seq_lens, ring_offset, B, Hq, Hkv, D, S, W, sm_scale,
+                                      out, out_dtype, lse, workspace, workspace_bytes, stream, nullptr);
+}
+
+spire_status spire_draft_sparse_attn_ex(const void *q, int32_t q_dtype, const spire_kv *sink,
+                                        const spire_kv *ring, const int32_t *seq_lens,
+                                        const int32_t *ring_offset, int32_t B, int32_t Hq,
+                                        int32_t Hkv, int32_t D, int32_t S, int32_t W, float sm_scale,
+                                        void *out, int32_t out_dtype, float *lse, void *workspace,
+                                        size_t workspace_bytes, hipStream_t stream,
+                                        const spire_launch_opts *opts) {
     g_err[0] = '\0';
-    spire_status s = common_checks(q, q_dtype, B, Hq, Hkv, D, 0, out, out_dtype, workspace);
+    if (opts != nullptr && opts->n_launches != nullptr) *opts->n_launches = 0;
+    spire_status s = check_opts(opts);
+    if (s != SPIRE_OK) return s;
+    s = common_checks(q, q_dtype, B, Hq, Hkv, D, 0, out, out_dtype, workspace);
     if (s != SPIRE_OK) return s;
     s = check_scale(sm_scale);
     if (s != SPIRE_OK) return s;
@@ -407,9 +445,9 @@ spire_status spire_draft_sparse_attn(const void *q, int32_t q_dtype, const spire
     const bool same_scales = ring->dtype != SPIRE_FP8_E4M3FN ||
                              (ring->k_scale == sink->k_scale && ring->v_scale == sink->v_scale);
     const bool mfma = (ring->dtype == SPIRE_BF16 || ring->dtype == SPIRE_FP8_E4M3FN) &&
-                      q_dtype == SPIRE_BF16 && D == 128 && p.R <= 80 && same_scales &&
+                      q_dtype == SPIRE_BF16 && D == 128 && p.R <= kMaxRows && same_scales &&
                       rows_aligned(ring) && rows_aligned(sink);
-    return run(p, mfma, workspace, workspace_bytes, stream, 2);
+    return run(p, mfma, workspace, workspace_bytes, stream, KID_DRAFT, opts);
 }
 
 // ---- token verification -------------------------------------------------------
@@ -426,7 +464,19 @@ spire_status spire_token_verify(const float *p_target, const float *q_draft,
                                 const float *u_sample, int32_t B, int32_t k, int32_t V,
                                 int32_t *n_accepted, int32_t *out_tokens, void *workspace,
                                 size_t workspace_bytes, hipStream_t stream) {
+    return spire_token_verify_ex(p_target, q_draft, draft_tokens, u_accept, u_sample, B, k, V, n_accepted,
+                                 out_tokens, workspace, workspace_bytes, stream, nullptr);
+}
+
+spire_status spire_token_verify_ex(const float *p_target, const float *q_draft,
+                                   const int32_t *draft_tokens, const float *u_accept,
+                                   const float *u_sample, int32_t B, int32_t k, int32_t V,
+                                   int32_t *n_accepted, int32_t *out_tokens, void *workspace,
+                                   size_t workspace_bytes, hipStream_t stream,
+                                   const spire_launch_opts *opts) {
     g_err[0] = '\0';
+    if (opts != nullptr && opts->n_launches != nullptr) *opts->n_launches = 0;
+    if (check_opts(opts) != SPIRE_OK) return SPIRE_ERR_INVALID_ARG;
     if (B < 0 || B > 65535) return fail(SPIRE_ERR_UNSUPPORTED, "B must be in [0, 65535] (got %d)", B);
     if (k < 0 || k > kTokenMaxK) return fail(SPIRE_ERR_UNSUPPORTED, "k must be in [0, %d] (got %d)", kTokenMaxK, k);
     if (V < 1 || V > kTokenMaxV) return fail(SPIRE_ERR_UNSUPPORTED, "V must be in [1, %d] (got %d)", kTokenMaxV, V);
@@ -458,9 +508,10 @@ spire_status spire_token_verify(const float *p_target, const float *q_draft,
     t.piece_sum = static_cast<uint64_t *>(workspace);
     t.nacc = reinterpret_cast<int32_t *>(static_cast<char *>(workspace) +
                                          align256((size_t)B * t.npieces * sizeof(uint64_t)));
-    hipError_t e = timed_call(4, stream, [&] { return launch_token_weights(t, stream); });
+    Recorder rec(opts);
+    hipError_t e = rec.run(KID_TOKEN_WEIGHTS, stream, [&] { return launch_token_weights(t, stream); });
     if (e != hipSuccess) return fail(SPIRE_ERR_HIP, "token weights launch: %s", hipGetErrorString(e));
-    e = timed_call(5, stream, [&] { return launch_token_select(t, stream); });
+    e = rec.run(KID_TOKEN_SELECT, stream, [&] { return launch_token_select(t, stream); });
     if (e != hipSuccess) return fail(SPIRE_ERR_HIP, "token select launch: %s", hipGetErrorString(e));
     return SPIRE_OK;
 }
@@ -497,9 +548,7 @@ spire_status spire_kv_append(const spire_kv *kv, const void *k_new, const void *
     if (!elems_aligned(kv)) return fail(SPIRE_ERR_INVALID_ARG, "kv storage not aligned to its element size");
     if ((int64_t)B * T * Hkv > ((int64_t)1 << 33)) return fail(SPIRE_ERR_UNSUPPORTED, "too many rows");
     const KvDev d = to_dev(kv);
-    hipError_t e = timed_call(6, stream, [&] {
-        return launch_kv_append(d, k_new, v_new, new_dtype, positions, B, T, Hkv, D, stream);
-    });
+    hipError_t e = launch_kv_append(d, k_new, v_new, new_dtype, positions, B, T, Hkv, D, stream);
     if (e != hipSuccess) return fail(SPIRE_ERR_HIP, "kv append launch: %s", hipGetErrorString(e));
     return SPIRE_OK;
 }
@@ -537,10 +586,8 @@ spire_status spire_draft_append(const spire_kv *sink, const spire_kv *ring, cons
     if ((spill_k == nullptr) != (spill_v == nullptr))
         return fail(SPIRE_ERR_INVALID_ARG, "give both spill_k and spill_v, or neither");
     const KvDev ds = to_dev(sink), dr = to_dev(ring);
-    hipError_t e = timed_call(7, stream, [&] {
-        return launch_draft_append(ds, dr, k_new, v_new, new_dtype, seq_lens, ring_offset, B, Hkv, D, S, W,
-                                   spill_k, spill_v, stream);
-    });
+    hipError_t e = launch_draft_append(ds, dr, k_new, v_new, new_dtype, seq_lens, ring_offset, B, Hkv, D, S, W,
+                                       spill_k, spill_v, stream);
     if (e != hipSuccess) return fail(SPIRE_ERR_HIP, "draft append launch: %s", hipGetErrorString(e));
     return SPIRE_OK;
 }
@@ -560,10 +607,8 @@ spire_status spire_draft_rollback(const spire_kv *sink, const spire_kv *ring, co
         ring_offset == nullptr)
         return fail(SPIRE_ERR_INVALID_ARG, "spill_k, spill_v, base_lens, n_accepted or ring_offset is NULL");
     const KvDev ds = to_dev(sink), dr = to_dev(ring);
-    hipError_t e = timed_call(8, stream, [&] {
-        return launch_draft_rollback(ds, dr, spill_k, spill_v, base_lens, n_accepted, steps, ring_offset, B, Hkv,
-                                     D, S, W, stream);
-    });
+    hipError_t e = launch_draft_rollback(ds, dr, spill_k, spill_v, base_lens, n_accepted, steps, ring_offset, B,
+                                         Hkv, D, S, W, stream);
     if (e != hipSuccess) return fail(SPIRE_ERR_HIP, "draft rollback launch: %s", hipGetErrorString(e));
     return SPIRE_OK;
 }
@@ -595,7 +640,7 @@ spire_status spire_feedback_memory(const void *x, int32_t x_dtype, const float *
     a.n_out = n_out;
     a.Lp1 = layers;
     a.Bd = (int64_t)B * d;
-    hipError_t e = timed_call(9, stream, [&] { return launch_feedback_memory(a, stream); });
+    hipError_t e = launch_feedback_memory(a, stream);
     if (e != hipSuccess) return fail(SPIRE_ERR_HIP, "feedback memory launch: %s", hipGetErrorString(e));
     return SPIRE_OK;
 }
@@ -610,51 +655,9 @@ spire_status spire_hbm_read_probe(const void *buf, size_t bytes, uint32_t *sink,
         return fail(SPIRE_ERR_INVALID_ARG, "buf must be 16-byte aligned and bytes a multiple of 16");
     if (((uintptr_t)sink & 3u) != 0) return fail(SPIRE_ERR_INVALID_ARG, "sink must be 4-byte aligned");
     if (bytes > (size_t)INT64_MAX) return fail(SPIRE_ERR_INVALID_ARG, "bytes too large");
-    hipError_t e = timed_call(10, stream, [&] { return launch_hbm_read(buf, (int64_t)bytes, sink, stream); });
+    hipError_t e = launch_hbm_read(buf, (int64_t)bytes, sink, stream);
     if (e != hipSuccess) return fail(SPIRE_ERR_HIP, "read probe launch: %s", hipGetErrorString(e));
     return SPIRE_OK;
-}
-
-spire_status spire_timing_enable(int32_t on) {
-    if (on) {
-        if (g_timing) return SPIRE_OK;
-        g_ev.resize(kTimingSlots);
-        for (auto &r : g_ev) {
-            if (hipEventCreate(&r.a) != hipSuccess || hipEventCreate(&r.b) != hipSuccess)
-                return fail(SPIRE_ERR_HIP, "hipEventCreate failed");
-        }
-        g_ev_next = 0;
-        g_ev_count = 0;
-        g_timing = true;
-    } else {
-        if (!g_timing) return SPIRE_OK;
-        for (auto &r : g_ev) {
-            (void)hipEventDestroy(r.a);
-            (void)hipEventDestroy(r.b);
-        }
-        g_ev.clear();
-        g_timing = false;
-    }
-    return SPIRE_OK;
-}
-
-int32_t spire_timing_collect(int32_t *kernel_ids, float *ms, int32_t max) {
-    if (!g_timing) return 0;
-    int written = 0;
-    const int first = (g_ev_next - g_ev_count + kTimingSlots) % kTimingSlots;
-    for (int i = 0; i < g_ev_count; ++i) {
-        TimingRec &r = g_ev[(first + i) % kTimingSlots];
-        if (hipEventSynchronize(r.b) != hipSuccess) continue;
-        float t = 0.f;
-        if (hipEventElapsedTime(&t, r.a, r.b) != hipSuccess) continue;
-        if (written < max) {
-            if (kernel_ids) kernel_ids[written] = r.id;
-            if (ms) ms[written] = t;
-            ++written;
-        }
-    }
-    g_ev_count = 0;
-    return written;
 }
 
 }  // extern "C"

@@ -171,6 +171,9 @@ constexpr int staged_waves(bool fp8, int nb) { return nb <= 2 || (fp8 && nb == 5
 constexpr int staged_wps(bool fp8, int nb) { return fp8 && nb > 2 && nb < 5 ? 2 : 1; }
 int staged_workers(int cus, int nb, bool fp8);
 hipError_t launch_combine(const Problem &p, const Plan &pl, hipStream_t st);
+// After a matrix-core verify call: recompute exactly the segments whose values
+// at keys [n - k, n) are not all finite (attn_generic.hip).
+hipError_t launch_tail_fix(const Problem &p, const Plan &pl, hipStream_t st);
 hipError_t launch_hbm_read(const void *buf, int64_t bytes, uint32_t *sink, hipStream_t st);
 
 // ---- token verification (token_verify.hip) -----------------------------------

@@ -26,12 +26,14 @@ STATUS = {0: "SPIRE_OK", 1: "SPIRE_ERR_INVALID_ARG", 2: "SPIRE_ERR_UNSUPPORTED",
 SYMBOLS = ["spire_verify_workspace_size", "spire_verify_attn", "spire_draft_workspace_size",
            "spire_draft_sparse_attn", "spire_token_verify_workspace_size", "spire_token_verify",
            "spire_kv_append", "spire_draft_append", "spire_draft_rollback", "spire_feedback_memory",
-           "spire_status_string", "spire_last_error", "spire_version", "spire_set_kernel_variant",
-           "spire_timing_enable", "spire_timing_collect", "spire_hbm_read_probe"]
+           "spire_hbm_read_probe", "spire_status_string", "spire_last_error", "spire_version",
+           "spire_verify_attn_ex", "spire_draft_sparse_attn_ex", "spire_token_verify_ex"]
 
+# kernel ids of the launches recorded through spire_launch_opts
 KERNEL_IDS = {0: "plan", 1: "verify_partial", 2: "draft_partial", 3: "combine",
-              4: "token_weights", 5: "token_select", 6: "kv_append", 7: "draft_append",
-              8: "draft_rollback", 9: "feedback_memory", 10: "hbm_read_probe"}
+              4: "token_weights", 5: "token_select", 11: "tail_check"}
+# kernel families (spire_launch_opts.kernel)
+KERNEL_AUTO, KERNEL_GENERIC, KERNEL_REGS, KERNEL_LDS = 0, 1, 2, 3
 HBM_PROBE_SINK_WORDS = 2048
 
 
@@ -48,6 +50,12 @@ class KV(C.Structure):
                 ("s_blk", C.c_int64), ("s_head", C.c_int64), ("s_tok", C.c_int64),
                 ("dtype", C.c_int32), ("page_size", C.c_int32), ("max_blocks", C.c_int32),
                 ("num_blocks", C.c_int32), ("capacity", C.c_int32), ("reserved", C.c_int32)]
+
+
+class LaunchOpts(C.Structure):
+    """struct spire_launch_opts"""
+    _fields_ = [("kernel", C.c_int32), ("max_launches", C.c_int32), ("events", C.c_void_p),
+                ("kernel_ids", C.c_void_p), ("n_launches", C.c_void_p), ("reserved", C.c_int32)]
 
 
 _lib = None
@@ -92,14 +100,14 @@ def load(path: Optional[str] = None):
     L.spire_last_error.restype = C.c_char_p
     L.spire_last_error.argtypes = []
     L.spire_version.restype = i32
-    L.spire_set_kernel_variant.restype = C.c_int
-    L.spire_set_kernel_variant.argtypes = [i32]
+    L.spire_verify_attn_ex.restype = C.c_int
+    L.spire_verify_attn_ex.argtypes = L.spire_verify_attn.argtypes + [C.POINTER(LaunchOpts)]
+    L.spire_draft_sparse_attn_ex.restype = C.c_int
+    L.spire_draft_sparse_attn_ex.argtypes = L.spire_draft_sparse_attn.argtypes + [C.POINTER(LaunchOpts)]
+    L.spire_token_verify_ex.restype = C.c_int
+    L.spire_token_verify_ex.argtypes = L.spire_token_verify.argtypes + [C.POINTER(LaunchOpts)]
     L.spire_hbm_read_probe.restype = C.c_int
     L.spire_hbm_read_probe.argtypes = [vp, sz, vp, sz, vp]
-    L.spire_timing_enable.restype = C.c_int
-    L.spire_timing_enable.argtypes = [i32]
-    L.spire_timing_collect.restype = i32
-    L.spire_timing_collect.argtypes = [vp, vp, i32]
     if path is None:
         _lib = L
     return L
@@ -159,11 +167,53 @@ def workspace(nbytes: int, device=None) -> torch.Tensor:
     return torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device or "cuda")
 
 
+class LaunchRecorder:
+    """Caller-owned HIP events the library records around each kernel one call
+    launches (spire_launch_opts): pass `rec.opts(kernel)` as `opts`, then
+    `rec.collect()` gives [(kernel name, ms)] of that call's launches."""
+
+    def __init__(self, max_launches: int = 8):
+        self.max = max_launches
+        self.events = [torch.cuda.Event(enable_timing=True) for _ in range(2 * max_launches)]
+        for e in self.events:       # torch creates the underlying HIP event on first record
+            e.record()
+        torch.cuda.synchronize()
+        self._handles = (C.c_void_p * (2 * max_launches))(*[e.cuda_event for e in self.events])
+        self._ids = (C.c_int32 * max_launches)()
+        self._n = C.c_int32(0)
+
+    def opts(self, kernel: int = 0) -> LaunchOpts:
+        o = LaunchOpts()
+        o.kernel, o.max_launches = kernel, self.max
+        o.events = C.cast(self._handles, C.c_void_p)
+        o.kernel_ids, o.n_launches = C.addressof(self._ids), C.addressof(self._n)
+        o.reserved = 0
+        return o
+
+    def collect(self):
+        """[(kernel name, ms)] of the recorded launches of the last call (synchronises)."""
+        torch.cuda.synchronize()
+        n = min(self._n.value, self.max)
+        return [(KERNEL_IDS.get(self._ids[i], str(self._ids[i])),
+                 self.events[2 * i].elapsed_time(self.events[2 * i + 1])) for i in range(n)]
+
+
+def _opts(kernel: int, opts: Optional[LaunchOpts]):
+    if opts is None and kernel == 0:
+        return None
+    if opts is None:
+        opts = LaunchOpts()
+        opts.kernel = kernel
+    return C.byref(opts)
+
+
 def verify_attn(q: torch.Tensor, kv: KV, kv_lens: torch.Tensor, Hkv: int, k: int,
                 sm_scale: float, out: Optional[torch.Tensor] = None,
                 lse: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,
-                out_dtype=torch.float32, with_lse: bool = True):
-    """spire_verify_attn.  q [B, k+1, Hq, D]; returns (out, lse)."""
+                out_dtype=torch.float32, with_lse: bool = True, kernel: int = 0,
+                opts: Optional[LaunchOpts] = None):
+    """spire_verify_attn (spire_verify_attn_ex with a kernel choice or launch
+    events).  q [B, k+1, Hq, D]; returns (out, lse)."""
     B, nq, Hq, D = q.shape
     assert nq == k + 1 and q.is_contiguous()
     if out is None:
@@ -173,9 +223,9 @@ def verify_attn(q: torch.Tensor, kv: KV, kv_lens: torch.Tensor, Hkv: int, k: int
     if ws is None:
         ws = workspace(verify_workspace_size(B, Hq, Hkv, D, k), q.device)
     lens = kv_lens if kv_lens.dtype == torch.int32 else kv_lens.to(torch.int32)
-    _check(load().spire_verify_attn(q.data_ptr(), _DT[q.dtype], C.byref(kv), lens.data_ptr(), B, Hq,
-                                    Hkv, D, k, float(sm_scale), out.data_ptr(), _DT[out.dtype],
-                                    _ptr(lse), ws.data_ptr(), ws.numel(), _stream()))
+    _check(load().spire_verify_attn_ex(q.data_ptr(), _DT[q.dtype], C.byref(kv), lens.data_ptr(), B, Hq,
+                                       Hkv, D, k, float(sm_scale), out.data_ptr(), _DT[out.dtype],
+                                       _ptr(lse), ws.data_ptr(), ws.numel(), _stream(), _opts(kernel, opts)))
     return out, lse
 
 
@@ -183,8 +233,9 @@ def draft_sparse_attn(q: torch.Tensor, sink: KV, ring: KV, seq_lens: torch.Tenso
                       ring_offset: torch.Tensor, S: int, W: int, sm_scale: float, Hkv: int,
                       out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None,
                       ws: Optional[torch.Tensor] = None, out_dtype=torch.float32,
-                      with_lse: bool = True):
-    """spire_draft_sparse_attn.  q [B, Hq, D]; returns (out, lse)."""
+                      with_lse: bool = True, kernel: int = 0, opts: Optional[LaunchOpts] = None):
+    """spire_draft_sparse_attn (the _ex form with a kernel choice or launch
+    events).  q [B, Hq, D]; returns (out, lse)."""
     B, Hq, D = q.shape
     assert q.is_contiguous()
     if out is None:
@@ -193,10 +244,11 @@ def draft_sparse_attn(q: torch.Tensor, sink: KV, ring: KV, seq_lens: torch.Tenso
         lse = torch.empty((B, Hq), dtype=torch.float32, device=q.device)
     if ws is None:
         ws = workspace(draft_workspace_size(B, Hq, Hkv, D), q.device)
-    _check(load().spire_draft_sparse_attn(q.data_ptr(), _DT[q.dtype], C.byref(sink), C.byref(ring),
-                                          seq_lens.data_ptr(), ring_offset.data_ptr(), B, Hq, Hkv,
-                                          D, S, W, float(sm_scale), out.data_ptr(), _DT[out.dtype],
-                                          _ptr(lse), ws.data_ptr(), ws.numel(), _stream()))
+    _check(load().spire_draft_sparse_attn_ex(q.data_ptr(), _DT[q.dtype], C.byref(sink), C.byref(ring),
+                                             seq_lens.data_ptr(), ring_offset.data_ptr(), B, Hq, Hkv,
+                                             D, S, W, float(sm_scale), out.data_ptr(), _DT[out.dtype],
+                                             _ptr(lse), ws.data_ptr(), ws.numel(), _stream(),
+                                             _opts(kernel, opts)))
     return out, lse
 
 
@@ -207,7 +259,7 @@ def token_verify_workspace_size(B, k, V) -> int:
 def token_verify(p: torch.Tensor, q: Optional[torch.Tensor], draft: Optional[torch.Tensor],
                  u_accept: Optional[torch.Tensor], u_sample: torch.Tensor,
                  n_accepted: Optional[torch.Tensor] = None, tokens: Optional[torch.Tensor] = None,
-                 ws: Optional[torch.Tensor] = None):
+                 ws: Optional[torch.Tensor] = None, opts: Optional[LaunchOpts] = None):
     """spire_token_verify.  p [B, k+1, V] fp32, q [B, k, V] fp32, draft [B, k]
     int32, u_accept [B, k] fp32, u_sample [B] fp32; returns (n_accepted [B],
     tokens [B, k+1]) as int32 tensors."""
@@ -224,11 +276,11 @@ def token_verify(p: torch.Tensor, q: Optional[torch.Tensor], draft: Optional[tor
         tokens = torch.empty((B, kp1), dtype=torch.int32, device=p.device)
     if ws is None:
         ws = workspace(token_verify_workspace_size(B, k, V), p.device)
-    _check(load().spire_token_verify(p.data_ptr(), _ptr(q) if k > 0 else None,
-                                     _ptr(draft) if k > 0 else None,
-                                     _ptr(u_accept) if k > 0 else None, u_sample.data_ptr(), B, k,
-                                     V, n_accepted.data_ptr(), tokens.data_ptr(), ws.data_ptr(),
-                                     ws.numel(), _stream()))
+    _check(load().spire_token_verify_ex(p.data_ptr(), _ptr(q) if k > 0 else None,
+                                        _ptr(draft) if k > 0 else None,
+                                        _ptr(u_accept) if k > 0 else None, u_sample.data_ptr(), B, k,
+                                        V, n_accepted.data_ptr(), tokens.data_ptr(), ws.data_ptr(),
+                                        ws.numel(), _stream(), _opts(0, opts)))
     return n_accepted, tokens
 
 
@@ -280,10 +332,6 @@ def feedback_memory(x: torch.Tensor, w: torch.Tensor, out: Optional[torch.Tensor
     return out
 
 
-def set_kernel_variant(variant: int):
-    _check(load().spire_set_kernel_variant(variant))
-
-
 def hbm_read_probe(buf: torch.Tensor, sink: Optional[torch.Tensor] = None) -> torch.Tensor:
     """spire_hbm_read_probe: stream `buf` (contiguous, 16-byte aligned, a
     multiple of 16 bytes) once; returns the int32 sink of XOR folds."""
@@ -294,15 +342,3 @@ def hbm_read_probe(buf: torch.Tensor, sink: Optional[torch.Tensor] = None) -> to
     _check(load().spire_hbm_read_probe(buf.data_ptr(), buf.numel() * buf.element_size(),
                                        sink.data_ptr(), sink.numel(), _stream()))
     return sink
-
-
-def timing_enable(on: bool):
-    _check(load().spire_timing_enable(1 if on else 0))
-
-
-def timing_collect(max_records: int = 4096):
-    """[(kernel name, ms)] of the launches recorded since the last collect."""
-    ids = (C.c_int32 * max_records)()
-    ms = (C.c_float * max_records)()
-    n = load().spire_timing_collect(C.addressof(ids), C.addressof(ms), max_records)
-    return [(KERNEL_IDS.get(ids[i], str(ids[i])), float(ms[i])) for i in range(n)]

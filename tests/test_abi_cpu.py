@@ -136,13 +136,64 @@ def test_draft_rejects_invalid_arguments(kw, status):
     assert draft(**kw) == status
 
 
-def test_kernel_variant_and_sizes():
+def test_invalid_sizes_give_zero_workspace():
     L = spire.load()
-    assert L.spire_set_kernel_variant(4) == INVALID
-    assert L.spire_set_kernel_variant(-1) == INVALID
-    assert L.spire_set_kernel_variant(0) == OK
     assert L.spire_verify_workspace_size(4, 30, 8, 128, 4) == 0
     assert L.spire_draft_workspace_size(4, 32, 0, 128) == 0
+
+
+def _opts(kernel=0, max_launches=0, events=None, reserved=0):
+    o = spire.LaunchOpts()
+    o.kernel, o.max_launches, o.events, o.reserved = kernel, max_launches, events, reserved
+    n = C.c_int32(-7)
+    o.n_launches = C.addressof(n)
+    return o, n
+
+
+@pytest.mark.parametrize("kw", [dict(kernel=4), dict(kernel=-1), dict(max_launches=-1),
+                                dict(max_launches=2), dict(reserved=1)])
+def test_invalid_launch_options_are_rejected(kw):
+    """Per-call options are checked before anything is enqueued (events NULL
+    with max_launches > 0, unknown kernel family, reserved field); the launch
+    count reads 0."""
+    L = spire.load()
+    for call in ("verify", "draft", "token"):
+        o, n = _opts(**kw)
+        if call == "verify":
+            rc = L.spire_verify_attn_ex(FAKE, spire.BF16, C.byref(kv()), FAKE, 2, 32, 8, 128, 4, 0.1, FAKE,
+                                        spire.F32, None, FAKE, 1 << 30, None, C.byref(o))
+        elif call == "draft":
+            rc = L.spire_draft_sparse_attn_ex(FAKE, spire.BF16, C.byref(kv(capacity=4)), C.byref(kv()), FAKE,
+                                              FAKE, 2, 32, 8, 128, 4, 64, 0.1, FAKE, spire.F32, None, FAKE,
+                                              1 << 30, None, C.byref(o))
+        else:
+            rc = L.spire_token_verify_ex(FAKE, FAKE, FAKE, FAKE, FAKE, 2, 4, 1000, FAKE, FAKE, FAKE, 1 << 20,
+                                         None, C.byref(o))
+        assert rc == INVALID, (call, kw)
+        assert n.value == 0
+        assert "opts" in L.spire_last_error().decode()
+
+
+def test_library_has_no_mutable_globals_besides_the_device_cache():
+    """The boundary is stateless: apart from the per-device compute-unit cache
+    (and its mutex) and the thread-local error message, the library's host code
+    keeps no writable data symbols."""
+    out = subprocess.run(["nm", "-C", "--defined-only", spire.LIB_PATH], capture_output=True, text=True,
+                         check=True).stdout
+    allowed = ("g_cus", "g_dev_mu", "g_err")
+    writable = []
+    for ln in out.splitlines():
+        parts = ln.split(None, 2)
+        if len(parts) != 3 or parts[1] not in ("B", "b", "D", "d"):
+            continue
+        name = parts[2]
+        if "(" in name.replace("(anonymous namespace)", ""):
+            continue  # host-side handles of the kernels, not state
+        if name.startswith(("spire", "(anonymous namespace)")):
+            writable.append(name)
+    assert any("g_cus" in w for w in writable)  # the scan sees the library's own data
+    bad = [w for w in writable if not any(a in w for a in allowed)]
+    assert not bad, bad
 
 
 def token(**kw):

@@ -12,7 +12,7 @@ import torch
 from paper_2504_06419_amd import spire
 from paper_2504_06419_amd import workloads as W
 from tests.gpu_helpers import (TOL, banner, lse_err, max_err, oracle_draft, oracle_verify,
-                               run_draft, run_verify, sample_ids)
+                               role_ids, run_draft, run_verify, sample_ids)
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda"
@@ -21,13 +21,12 @@ NW = W.named_workloads()
 
 @pytest.fixture(params=[0, 1, 2, 3], ids=["auto", "generic", "mfma_regs", "mfma_lds"])
 def variant(request):
-    spire.set_kernel_variant(request.param)
-    yield request.param
-    spire.set_kernel_variant(0)
+    """The kernel family each call asks for (spire_launch_opts.kernel)."""
+    return request.param
 
 
-def _check_verify(inp, tol, seq_ids=None, out_dtype=torch.float32):
-    out, lse = run_verify(inp, out_dtype=out_dtype)
+def _check_verify(inp, tol, seq_ids=None, out_dtype=torch.float32, kernel=0):
+    out, lse = run_verify(inp, out_dtype=out_dtype, kernel=kernel)
     ref_o, ref_l = oracle_verify(inp, seq_ids)
     if seq_ids is not None:
         out, lse = out[seq_ids], lse[seq_ids]
@@ -37,8 +36,8 @@ def _check_verify(inp, tol, seq_ids=None, out_dtype=torch.float32):
     return out, lse
 
 
-def _check_draft(inp, step, tol, seq_ids=None):
-    out, lse = run_draft(inp, step)
+def _check_draft(inp, step, tol, seq_ids=None, kernel=0):
+    out, lse = run_draft(inp, step, kernel=kernel)
     ref_o, ref_l = oracle_draft(inp, step, seq_ids)
     if seq_ids is not None:
         out, lse = out[seq_ids], lse[seq_ids]
@@ -54,7 +53,7 @@ def test_tiny_f32_verify(variant):
     banner(f"tiny_f32 verify variant={variant}")
     spec = NW["tiny_f32"]["verify"]
     inp = W.make_verify_inputs(spec, W.MASTER_SEED + 0, device=DEV)
-    _check_verify(inp, TOL["f32"])
+    _check_verify(inp, TOL["f32"], kernel=variant)
 
 
 def test_tiny_f32_draft_steps(variant):
@@ -63,7 +62,7 @@ def test_tiny_f32_draft_steps(variant):
     inp = W.make_draft_inputs(spec, W.MASTER_SEED + 0, device=DEV)
     for step in range(spec.steps):
         W.write_step_token(inp, step)
-        _check_draft(inp, step, TOL["f32"])
+        _check_draft(inp, step, TOL["f32"], kernel=variant)
 
 
 def test_tiny_f32_draft_on_target_cache_view():
@@ -93,13 +92,17 @@ def test_tiny_f32_draft_on_target_cache_view():
 # ---------------------------------------------------------------------------
 @pytest.mark.parametrize("kv_dtype", ["bf16", "fp8"])
 @pytest.mark.parametrize("ps", [0, 16, 32])
-@pytest.mark.parametrize("k,g", [(0, 1), (1, 4), (4, 4), (7, 8), (8, 8), (3, 2)])
+@pytest.mark.parametrize("k,g", [(0, 1), (1, 4), (4, 4), (7, 8), (8, 8), (3, 2),
+                                 (10, 1), (12, 6), (10, 8), (15, 8)])
 def test_verify_small_shapes(variant, kv_dtype, ps, k, g):
+    """Up to (k+1) * g = 128 rows per KV head (k = 15, 8 query heads per KV
+    head): 1-2 row blocks on the register-staged kernel, 3-8 on the LDS-staged
+    one (one wave, or two sharing the stage ring)."""
     banner(f"verify small {kv_dtype} ps={ps} k={k} g={g} variant={variant}")
     spec = W.VerifySpec(B=6, Hq=2 * g, Hkv=2, D=128, k=k, ctx_lo=1, ctx_hi=300, kv_dtype=kv_dtype,
                         page_size=ps, spare_pages=3, log_uniform=True)
     inp = W.make_verify_inputs(spec, 1000 + 13 * k + g + ps, device=DEV)
-    _check_verify(inp, TOL[kv_dtype])
+    _check_verify(inp, TOL[kv_dtype], kernel=variant)
 
 
 @pytest.mark.parametrize("kv_dtype", ["bf16", "fp8"])
@@ -118,7 +121,7 @@ def test_verify_growing_scores(variant, kv_dtype, k, g):
     kf = kc.float() * ramp
     kf[:, :, 397::811] *= 3.0                           # spikes
     kc.copy_(kf.clamp(-448.0, 448.0).to(kc.dtype))
-    _check_verify(inp, TOL[kv_dtype])
+    _check_verify(inp, TOL[kv_dtype], kernel=variant)
 
 
 @pytest.mark.parametrize("D", [64, 128])
@@ -127,7 +130,7 @@ def test_verify_fp32_and_head_dims(variant, D):
     spec = W.VerifySpec(B=3, Hq=8, Hkv=2, D=D, k=4, ctx_lo=30, ctx_hi=200, kv_dtype="f32",
                         q_dtype="f32", page_size=16, spare_pages=2)
     inp = W.make_verify_inputs(spec, 77 + D, device=DEV)
-    _check_verify(inp, TOL["f32"])
+    _check_verify(inp, TOL["f32"], kernel=variant)
 
 
 def test_verify_bf16_head_dim_64():
@@ -151,11 +154,9 @@ def test_verify_degenerate_lengths():
     inp = W.make_verify_inputs(spec, 8, device=DEV)
     inp.kv_lens = torch.tensor([5, 3, 0, 1, 5], dtype=torch.int32, device=DEV)
     for v in (0, 1):
-        spire.set_kernel_variant(v)
-        out, lse = run_verify(inp)
+        out, lse = run_verify(inp, kernel=v)
         ref_o, ref_l = oracle_verify(inp)
         assert max_err(out, ref_o) <= TOL["bf16"] and lse_err(lse, ref_l) <= TOL["bf16"]
-    spire.set_kernel_variant(0)
 
 
 def test_verify_lengths_beyond_capacity_are_clamped():
@@ -206,7 +207,7 @@ def test_draft_small_shapes(variant, kv_dtype, S, Wn, lo, hi):
     inp = W.make_draft_inputs(spec, 2000 + S + Wn + lo, device=DEV)
     for step in range(spec.steps):
         W.write_step_token(inp, step)
-        _check_draft(inp, step, TOL[kv_dtype])
+        _check_draft(inp, step, TOL[kv_dtype], kernel=variant)
 
 
 @pytest.mark.parametrize("kv_dtype", ["bf16", "fp8"])
@@ -221,7 +222,7 @@ def test_draft_group_sizes(variant, kv_dtype, g):
     inp = W.make_draft_inputs(spec, 3000 + g, device=DEV)
     for step in range(spec.steps):
         W.write_step_token(inp, step)
-        _check_draft(inp, step, TOL[kv_dtype])
+        _check_draft(inp, step, TOL[kv_dtype], kernel=variant)
 
 
 # ---------------------------------------------------------------------------
@@ -247,10 +248,8 @@ def test_paged_equals_contiguous_on_gpu():
         W.VerifySpec(B=5, Hq=16, Hkv=4, D=128, k=3, ctx_lo=20, ctx_hi=900, page_size=ps), 12,
         device=DEV, keep_logical=True)
     a, b = mk(0), mk(16)
-    spire.set_kernel_variant(1)        # same arithmetic on both layouts: bitwise equal
-    oa, la = run_verify(a)
-    ob, lb = run_verify(b)
-    spire.set_kernel_variant(0)
+    oa, la = run_verify(a, kernel=1)   # same arithmetic on both layouts: bitwise equal
+    ob, lb = run_verify(b, kernel=1)
     assert torch.equal(oa, ob) and torch.equal(la, lb)
     oc, lc = run_verify(b)             # matrix-core path on the paged layout
     assert (oa - oc).abs().max().item() <= TOL["bf16"]
@@ -259,13 +258,17 @@ def test_paged_equals_contiguous_on_gpu():
 # ---------------------------------------------------------------------------
 # full-size workloads (sampled sequences against the oracle)
 # ---------------------------------------------------------------------------
+def _finite_everywhere(inp):
+    out, lse = run_verify(inp)
+    assert torch.isfinite(out).all().item() and torch.isfinite(lse).all().item()
+
+
 def test_verify_bf16_B64_L8192():
     banner("verify_bf16_B64_L8192")
     spec = NW["verify_bf16_B64_L8192"]["verify"]
     inp = W.make_verify_inputs(spec, W.MASTER_SEED + 1, device=DEV)
-    out, _ = _check_verify(inp, TOL["bf16"], seq_ids=[0, 17, 63])
-    full, _ = run_verify(inp)
-    assert torch.isfinite(full).all()
+    _check_verify(inp, TOL["bf16"], seq_ids=sorted({17} | set(role_ids(inp, seed=1))))
+    _finite_everywhere(inp)
 
 
 def test_draft_bf16_B64_S4_W2048():
@@ -281,8 +284,8 @@ def test_verify_varlen_paged_bf16_B256():
     banner("verify_varlen_paged_bf16_B256")
     spec = NW["verify_varlen_paged_bf16_B256"]["verify"]
     inp = W.make_verify_inputs(spec, W.MASTER_SEED + 3, device=DEV)
-    ids = sample_ids(inp.kv_lens.tolist(), 6, seed=3)
-    _check_verify(inp, TOL["bf16"], seq_ids=ids)
+    _check_verify(inp, TOL["bf16"], seq_ids=role_ids(inp, seed=3))
+    _finite_everywhere(inp)
 
 
 def test_round_fp8_B512_k8():
@@ -292,19 +295,21 @@ def test_round_fp8_B512_k8():
     for step in range(wl["draft"].steps):
         W.write_step_token(d, step)
         _check_draft(d, step, TOL["fp8"], seq_ids=sample_ids(d.base_lens, 3, seed=step))
+        out, lse = run_draft(d, step)
+        assert torch.isfinite(out).all().item() and torch.isfinite(lse).all().item()
     del d
     torch.cuda.empty_cache()
     inp = W.make_verify_inputs(wl["verify"], W.MASTER_SEED + 4, device=DEV)
-    ids = sample_ids(inp.kv_lens.tolist(), 4, seed=4)
-    _check_verify(inp, TOL["fp8"], seq_ids=ids)
+    _check_verify(inp, TOL["fp8"], seq_ids=role_ids(inp, seed=4))
+    _finite_everywhere(inp)
 
 
 def test_verify_tp8shard_fp8_B512_k8():
     banner("verify_tp8shard_fp8_B512_k8: one tensor-parallel shard of the fp8 verify")
     name = "verify_tp8shard_fp8_B512_k8"
     inp = W.make_verify_inputs(NW[name]["verify"], W.MASTER_SEED + W.WORKLOAD_INDEX[name], device=DEV)
-    ids = sample_ids(inp.kv_lens.tolist(), 6, seed=9)
-    _check_verify(inp, TOL["fp8"], seq_ids=ids)
+    _check_verify(inp, TOL["fp8"], seq_ids=role_ids(inp, seed=9))
+    _finite_everywhere(inp)
 
 
 # (kv dtype, k, query heads per KV head, phantom positions per segment):
@@ -354,3 +359,61 @@ def test_plan_partition_invariants(kv_dtype, k, g, seg_cost):
         assert prefix[b].item() * units + u * tiles[b] + t == b0
         covered += b1 - b0
     assert covered == T
+
+
+# ---------------------------------------------------------------------------
+# fp8 draft views with scales of their own; launch records
+# ---------------------------------------------------------------------------
+def test_draft_fp8_sink_and_ring_with_their_own_scales(variant):
+    """The header lets the sink and ring fp8 views carry different per-head
+    scales; each key is dequantised with its own view's scales."""
+    banner(f"draft fp8 with separate sink / ring scales variant={variant}")
+    spec = W.DraftSpec(B=6, Hq=16, Hkv=2, D=128, S=4, W=96, steps=2, ctx_lo=1, ctx_hi=400,
+                       kv_dtype="fp8")
+    inp = W.make_draft_inputs(spec, 3100, device=DEV)
+    sk = (inp.k_scale * torch.tensor([3.0, 0.25], device=DEV)).contiguous()
+    sv = (inp.v_scale * torch.tensor([0.5, 4.0], device=DEV)).contiguous()
+    sink = spire.kv_view(inp.sink_k, inp.sink_v, k_scale=sk, v_scale=sv)
+    ring = spire.kv_view(inp.ring_k, inp.ring_v, k_scale=inp.k_scale, v_scale=inp.v_scale)
+    from oracle import oracle as O
+    for step in range(spec.steps):
+        W.write_step_token(inp, step)
+        out, lse = spire.draft_sparse_attn(inp.q[step].contiguous(), sink, ring, inp.seq_lens(step),
+                                           inp.ring_offset, spec.S, spec.W, inp.sm_scale, spec.Hkv,
+                                           kernel=variant)
+        torch.cuda.synchronize()
+        ref_o, ref_l = O.draft(inp.q[step], inp.sink_k, inp.sink_v, inp.ring_k, inp.ring_v,
+                               inp.seq_lens(step), inp.ring_offset, spec.S, spec.W, inp.sm_scale,
+                               inp.k_scale, inp.v_scale, sink_k_scale=sk, sink_v_scale=sv)
+        same, _ = O.draft(inp.q[step], inp.sink_k, inp.sink_v, inp.ring_k, inp.ring_v,
+                          inp.seq_lens(step), inp.ring_offset, spec.S, spec.W, inp.sm_scale,
+                          inp.k_scale, inp.v_scale)
+        assert np.max(np.abs(ref_o - same)) > 1e-2          # the scales matter
+        eo, el = max_err(out, ref_o), lse_err(lse, ref_l)
+        print(f"  step {step}: max|out-oracle|={eo:.3e} max|lse-oracle|={el:.3e}", flush=True)
+        assert eo <= TOL["fp8"] and el <= TOL["fp8"]
+
+
+@pytest.mark.parametrize("kv_dtype,k,g,kernel,expect", [
+    ("bf16", 4, 4, 0, ["verify_partial", "combine", "tail_check"]),            # register-staged
+    ("fp8", 8, 8, 0, ["plan", "verify_partial", "combine", "tail_check"]),     # LDS-staged
+    ("bf16", 4, 4, 1, ["plan", "verify_partial", "combine"]),                  # generic
+])
+def test_launch_records(kv_dtype, k, g, kernel, expect):
+    """spire_launch_opts: the caller's events bracket each launch of the call, in
+    order, with its kernel id; the results equal those of the plain call."""
+    banner(f"launch records {kv_dtype} k={k} g={g} kernel={kernel}")
+    spec = W.VerifySpec(B=5, Hq=2 * g, Hkv=2, D=128, k=k, ctx_lo=100, ctx_hi=3000, kv_dtype=kv_dtype,
+                        page_size=16)
+    inp = W.make_verify_inputs(spec, 15, device=DEV)
+    rec = spire.LaunchRecorder(8)
+    kv = spire.kv_view(inp.k_cache, inp.v_cache, inp.block_table, 16, inp.k_scale, inp.v_scale)
+    out, lse = spire.verify_attn(inp.q, kv, inp.kv_lens, spec.Hkv, k, inp.sm_scale, opts=rec.opts(kernel))
+    recs = rec.collect()
+    assert [name for name, _ in recs] == expect
+    assert all(ms >= 0.0 for _, ms in recs)
+    ref_o, ref_l = run_verify(inp, kernel=kernel)
+    assert torch.equal(out, ref_o) and torch.equal(lse, ref_l)
+    small = spire.LaunchRecorder(1)                     # launches beyond max_launches are not recorded
+    spire.verify_attn(inp.q, kv, inp.kv_lens, spec.Hkv, k, inp.sm_scale, opts=small.opts(kernel))
+    assert [name for name, _ in small.collect()] == expect[:1] and small._n.value == len(expect)

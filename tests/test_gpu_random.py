@@ -31,9 +31,9 @@ def _verify_case(seed):
     rng = random.Random(seed)
     kv_dtype = rng.choice(["bf16", "bf16", "fp8", "fp8", "f32"])
     D = 128 if kv_dtype != "f32" else rng.choice([64, 128])
-    k = rng.randrange(0, 9)
+    k = rng.randrange(0, 16)
     g = rng.choice([1, 2, 3, 4, 6, 8])
-    while (k + 1) * g > 80:
+    while (k + 1) * g > 128:
         g //= 2
     Hkv = rng.choice([1, 2, 4, 8])
     B = rng.randrange(1, 49)
@@ -67,19 +67,12 @@ def _draft_case(seed):
     return spec, variant
 
 
-@pytest.fixture
-def restore_variant():
-    yield
-    spire.set_kernel_variant(0)
-
-
 @pytest.mark.parametrize("seed", range(CASES))
-def test_random_verify(seed, restore_variant):
+def test_random_verify(seed):
     spec, variant = _verify_case(seed)
     banner(f"random verify seed={seed} variant={variant} {spec}")
-    spire.set_kernel_variant(variant)
     inp = W.make_verify_inputs(spec, 5000 + seed, device=DEV)
-    out, lse = run_verify(inp)
+    out, lse = run_verify(inp, kernel=variant)
     ids = _sample(inp.kv_lens.tolist(), random.Random(seed))
     ref_o, ref_l = oracle_verify(inp, ids)
     eo, el = max_err(out[ids], ref_o), lse_err(lse[ids], ref_l)
@@ -89,14 +82,13 @@ def test_random_verify(seed, restore_variant):
 
 
 @pytest.mark.parametrize("seed", range(CASES))
-def test_random_draft(seed, restore_variant):
+def test_random_draft(seed):
     spec, variant = _draft_case(seed)
     banner(f"random draft seed={seed} variant={variant} {spec}")
-    spire.set_kernel_variant(variant)
     inp = W.make_draft_inputs(spec, 7000 + seed, device=DEV)
     for step in range(spec.steps):
         W.write_step_token(inp, step)
-        out, lse = run_draft(inp, step)
+        out, lse = run_draft(inp, step, kernel=variant)
         ids = _sample(inp.seq_lens(step).tolist(), random.Random(seed + step))
         ref_o, ref_l = oracle_draft(inp, step, ids)
         eo, el = max_err(out[ids], ref_o), lse_err(lse[ids], ref_l)
