@@ -141,6 +141,28 @@ spire_status spire_verify_attn(const void *q, int32_t q_dtype, const spire_kv *k
                                int32_t out_dtype, float *lse, void *workspace,
                                size_t workspace_bytes, hipStream_t stream);
 
+/*
+ * spire_verify_attn for callers that cannot allocate (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): the same
+ * arguments without a workspace, the same kernels and results.  Its scratch
+ * memory (the work partition and the partial results of split segments) is an
+ * 80 MiB array of the library in device memory, one per device, held from the
+ * library's load until the process ends; the first call on a device looks up
+ * that device's copy.  A call whose scratch need, spire_verify_workspace_size
+ * of the kernel it takes, exceeds it returns SPIRE_ERR_UNSUPPORTED and
+ * enqueues nothing (on a 256-CU MI355X at head_dim 128 that is fp8 K/V with 80
+ * rows per KV head, (k+1) * Hq / Hkv = 80; the 72 rows of k = 8 with 8 query
+ * heads per KV head need 72.6 MiB).
+ * The call allocates and frees nothing.  Every call on a device shares its
+ * array: calls that may overlap on one device (several streams or host
+ * threads) race and must be ordered by the caller; calls in order on one
+ * stream are safe.  The array needs no clearing between calls.
+ */
+spire_status spire_verify_attn_noalloc(const void *q, int32_t q_dtype, const spire_kv *kv,
+                                       const int32_t *kv_lens, int32_t B, int32_t Hq, int32_t Hkv,
+                                       int32_t D, int32_t k, float sm_scale, void *out,
+                                       int32_t out_dtype, float *lse, hipStream_t stream);
+
 /* Bytes of workspace spire_draft_sparse_attn needs (0 on invalid sizes). */
 size_t spire_draft_workspace_size(int32_t B, int32_t Hq, int32_t Hkv, int32_t D);
 

@@ -48,6 +48,32 @@ int device_cus(int *cus_out) {
     return 0;
 }
 
+// ---- library-owned scratch of the entry point that allocates nothing ---------
+// spire_verify_attn_noalloc runs the kernels of spire_verify_attn with this
+// array as their workspace.  Each device holds its own copy from the library's
+// load until the process ends.  In host code `scratch` names a host-side
+// stand-in, not device memory: only the address hipGetSymbolAddress returns
+// for the current device may reach a kernel.
+constexpr size_t kScratchBytes = (size_t)80 << 20;
+static __device__ __align__(256) uint8_t scratch[kScratchBytes];
+void *g_scratch[kMaxDevices] = {nullptr};  // device address of `scratch`, set once per device
+
+spire_status scratch_address(void **out) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices)
+        return fail(SPIRE_ERR_HIP, "cannot query the current HIP device");
+    std::lock_guard<std::mutex> lock(g_dev_mu);
+    if (g_scratch[dev] == nullptr) {
+        void *ptr = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || ptr == nullptr)
+            return fail(SPIRE_ERR_HIP, "hipGetSymbolAddress(scratch) on device %d: %s", dev, hipGetErrorString(e));
+        g_scratch[dev] = ptr;
+    }
+    *out = g_scratch[dev];
+    return SPIRE_OK;
+}
+
 // ---- workspace layout -------------------------------------------------------
 struct Layout {
     size_t nkeys, prefix, wstart, part_lse, part_o, total;
@@ -222,7 +248,7 @@ bool use_staged(const Problem &p, int kernel) {
 }
 
 spire_status run(Problem &p, bool use_mfma, void *workspace, size_t ws_bytes, hipStream_t stream,
-                 int partial_id, const spire_launch_opts *opts) {
+                 int partial_id, const spire_launch_opts *opts, bool lib_scratch = false) {
     int cus = 0;
     if (device_cus(&cus) != 0) return fail(SPIRE_ERR_HIP, "cannot query the current HIP device");
     const int kernel = opts != nullptr ? opts->kernel : 0;
@@ -249,6 +275,10 @@ spire_status run(Problem &p, bool use_mfma, void *workspace, size_t ws_bytes, hi
         return fail(SPIRE_ERR_UNSUPPORTED, "%d workers exceed the combine's limit of %d", pl.workers,
                     kCombineMaxWorkers);
     const Layout L = layout(p.B, pl.rows, p.D, pl.workers);
+    if (ws_bytes < L.total && lib_scratch)
+        return fail(SPIRE_ERR_UNSUPPORTED,
+                    "this call needs %zu bytes of scratch; the no-allocation entry point holds %zu per device "
+                    "(use spire_verify_attn with a workspace)", L.total, ws_bytes);
     if (ws_bytes < L.total)
         return fail(SPIRE_ERR_WORKSPACE, "workspace has %zu bytes, needs %zu", ws_bytes, L.total);
     char *ws = static_cast<char *>(workspace);
@@ -335,6 +365,13 @@ spire_status spire_verify_attn(const void *q, int32_t q_dtype, const spire_kv *k
                                 workspace, workspace_bytes, stream, nullptr);
 }
 
+static spire_status verify_impl(const void *q, int32_t q_dtype, const spire_kv *kv,
+                                const int32_t *kv_lens, int32_t B, int32_t Hq, int32_t Hkv,
+                                int32_t D, int32_t k, float sm_scale, void *out,
+                                int32_t out_dtype, float *lse, void *workspace,
+                                size_t workspace_bytes, hipStream_t stream,
+                                const spire_launch_opts *opts, bool lib_scratch);
+
 spire_status spire_verify_attn_ex(const void *q, int32_t q_dtype, const spire_kv *kv,
                                   const int32_t *kv_lens, int32_t B, int32_t Hq, int32_t Hkv,
                                   int32_t D, int32_t k, float sm_scale, void *out,
@@ -342,6 +379,30 @@ spire_status spire_verify_attn_ex(const void *q, int32_t q_dtype, const spire_kv
                                   size_t workspace_bytes, hipStream_t stream,
                                   const spire_launch_opts *opts) {
     g_err[0] = '\0';
+    return verify_impl(q, q_dtype, kv, kv_lens, B, Hq, Hkv, D, k, sm_scale, out, out_dtype, lse, workspace,
+                       workspace_bytes, stream, opts, false);
+}
+
+spire_status spire_verify_attn_noalloc(const void *q, int32_t q_dtype, const spire_kv *kv,
+                                       const int32_t *kv_lens, int32_t B, int32_t Hq, int32_t Hkv,
+                                       int32_t D, int32_t k, float sm_scale, void *out,
+                                       int32_t out_dtype, float *lse, hipStream_t stream) {
+    g_err[0] = '\0';
+    void *ws = nullptr;
+    if (B > 0) {
+        const spire_status s = scratch_address(&ws);
+        if (s != SPIRE_OK) return s;
+    }
+    return verify_impl(q, q_dtype, kv, kv_lens, B, Hq, Hkv, D, k, sm_scale, out, out_dtype, lse, ws,
+                       B > 0 ? kScratchBytes : 0, stream, nullptr, true);
+}
+
+static spire_status verify_impl(const void *q, int32_t q_dtype, const spire_kv *kv,
+                                const int32_t *kv_lens, int32_t B, int32_t Hq, int32_t Hkv,
+                                int32_t D, int32_t k, float sm_scale, void *out,
+                                int32_t out_dtype, float *lse, void *workspace,
+                                size_t workspace_bytes, hipStream_t stream,
+                                const spire_launch_opts *opts, bool lib_scratch) {
     if (opts != nullptr && opts->n_launches != nullptr) *opts->n_launches = 0;
     spire_status s = check_opts(opts);
     if (s != SPIRE_OK) return s;
@@ -382,7 +443,7 @@ spire_status spire_verify_attn_ex(const void *q, int32_t q_dtype, const spire_kv
             : (kv->capacity >= 1);
     const bool mfma = (kv->dtype == SPIRE_BF16 || kv->dtype == SPIRE_FP8_E4M3FN) &&
                       q_dtype == SPIRE_BF16 && D == 128 && p.R <= kMaxRows && layout_ok && rows_aligned(kv);
-    return run(p, mfma, workspace, workspace_bytes, stream, KID_VERIFY, opts);
+    return run(p, mfma, workspace, workspace_bytes, stream, KID_VERIFY, opts, lib_scratch);
 }
 
 spire_status spire_draft_sparse_attn(const void *q, int32_t q_dtype, const spire_kv *sink,

@@ -23,7 +23,8 @@ STATUS = {0: "SPIRE_OK", 1: "SPIRE_ERR_INVALID_ARG", 2: "SPIRE_ERR_UNSUPPORTED",
           3: "SPIRE_ERR_WORKSPACE", 4: "SPIRE_ERR_HIP"}
 
 # exported symbols, in the order include/spire.h declares them
-SYMBOLS = ["spire_verify_workspace_size", "spire_verify_attn", "spire_draft_workspace_size",
+SYMBOLS = ["spire_verify_workspace_size", "spire_verify_attn", "spire_verify_attn_noalloc",
+           "spire_draft_workspace_size",
            "spire_draft_sparse_attn", "spire_token_verify_workspace_size", "spire_token_verify",
            "spire_kv_append", "spire_draft_append", "spire_draft_rollback", "spire_feedback_memory",
            "spire_hbm_read_probe", "spire_status_string", "spire_last_error", "spire_version",
@@ -76,6 +77,9 @@ def load(path: Optional[str] = None):
     L.spire_verify_attn.restype = C.c_int
     L.spire_verify_attn.argtypes = [vp, i32, C.POINTER(KV), vp, i32, i32, i32, i32, i32, C.c_float,
                                     vp, i32, vp, vp, sz, vp]
+    L.spire_verify_attn_noalloc.restype = C.c_int
+    L.spire_verify_attn_noalloc.argtypes = [vp, i32, C.POINTER(KV), vp, i32, i32, i32, i32, i32, C.c_float,
+                                            vp, i32, vp, vp]
     L.spire_draft_workspace_size.restype = sz
     L.spire_draft_workspace_size.argtypes = [i32] * 4
     L.spire_draft_sparse_attn.restype = C.c_int
@@ -226,6 +230,20 @@ def verify_attn(q: torch.Tensor, kv: KV, kv_lens: torch.Tensor, Hkv: int, k: int
     _check(load().spire_verify_attn_ex(q.data_ptr(), _DT[q.dtype], C.byref(kv), lens.data_ptr(), B, Hq,
                                        Hkv, D, k, float(sm_scale), out.data_ptr(), _DT[out.dtype],
                                        _ptr(lse), ws.data_ptr(), ws.numel(), _stream(), _opts(kernel, opts)))
+    return out, lse
+
+
+def verify_attn_noalloc(q: torch.Tensor, kv: KV, kv_lens: torch.Tensor, Hkv: int, k: int,
+                        sm_scale: float, out: torch.Tensor, lse: Optional[torch.Tensor] = None):
+    """spire_verify_attn_noalloc: the verify call with the library's own
+    scratch instead of a workspace; the caller passes the outputs
+    (out [B, k+1, Hq, D] f32 or bf16, lse [B, k+1, Hq] f32 or None)."""
+    B, nq, Hq, D = q.shape
+    assert nq == k + 1 and q.is_contiguous() and out.is_contiguous()
+    lens = kv_lens if kv_lens.dtype == torch.int32 else kv_lens.to(torch.int32)
+    _check(load().spire_verify_attn_noalloc(q.data_ptr(), _DT[q.dtype], C.byref(kv), lens.data_ptr(), B, Hq,
+                                            Hkv, D, k, float(sm_scale), out.data_ptr(), _DT[out.dtype],
+                                            _ptr(lse), _stream()))
     return out, lse
 
 
