@@ -200,7 +200,7 @@ size_t spire_token_verify_workspace_size(int32_t B, int32_t k, int32_t V);
 /*
  * Token verification of one speculation round: the modified rejection
  * sampling that follows the target's verify pass and makes the accepted
- * tokens follow the target's distribution (paper Sec. 1 and Sec. 7; Table 1:
+ * tokens follow the target's distribution (paper Sec. 1 and Sec. 6; Table 1:
  * a round emits 1..k+1 tokens, 0..k accepted before the first rejection).
  * For each sequence b:
  *   n = the number of leading draft tokens x_i (i < k) with
@@ -332,8 +332,9 @@ spire_status spire_feedback_memory(const void *x, int32_t x_dtype, const float *
 spire_status spire_hbm_read_probe(const void *buf, size_t bytes, uint32_t *sink, size_t sink_words,
                                   hipStream_t stream);
 
-/* Human-readable name of a status code (static string, never NULL). */
-const char *spire_status_string(spire_status status);
+/* Human-readable name of a status code (static string, never NULL); any
+ * value is accepted, unknown ones give "SPIRE_ERR_UNKNOWN". */
+const char *spire_status_string(int32_t status);
 
 /* Detail message of the last non-OK status returned on the calling thread
  * (thread-local static storage, "" if none). */

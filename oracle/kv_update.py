@@ -125,7 +125,10 @@ def to_storage(x: np.ndarray, dtype: str, scale: float = 1.0) -> np.ndarray:
     if dtype == "bf16":
         return np.array([round_bf16_bits(v) for v in x], dtype=np.uint16)
     if dtype == "fp8":
-        y = (x / np.float32(scale)).astype(np.float32)     # fp32 IEEE division
+        # fp32 IEEE division; a quotient beyond the fp32 range becomes +-inf,
+        # which (like every magnitude of 448 and above) saturates to +-448 below
+        with np.errstate(over="ignore"):
+            y = (x / np.float32(scale)).astype(np.float32)
         return np.array([round_e4m3fn(float(v)) for v in y], dtype=np.uint8)
     raise ValueError(dtype)
 

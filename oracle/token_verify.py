@@ -4,7 +4,7 @@ Only the test suite, the package smoke check and the benchmark's CPU-baseline
 leg use this module; the HIP library never does.  It is a plain per-sequence
 statement of the token verification step that follows the target's parallel
 verify pass (paper Sec. 1: accepted draft tokens are guaranteed to follow the
-target's distribution thanks to a modified rejection sampling scheme; Sec. 7:
+target's distribution thanks to a modified rejection sampling scheme; Sec. 6:
 the experiments use token verification; Table 1's caption: a round emits
 between 1 and k+1 tokens, 0..k of them accepted before the first rejection).
 The scheme itself is the published one the paper cites (Leviathan et al. 2023,

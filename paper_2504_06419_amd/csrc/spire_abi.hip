@@ -326,7 +326,7 @@ extern "C" {
 
 int32_t spire_version(void) { return SPIRE_VERSION; }
 
-const char *spire_status_string(spire_status s) {
+const char *spire_status_string(int32_t s) {
     switch (s) {
     case SPIRE_OK: return "SPIRE_OK";
     case SPIRE_ERR_INVALID_ARG: return "SPIRE_ERR_INVALID_ARG";

@@ -6,7 +6,7 @@
 // norm(max(0, p_{n+1} - q_{n+1})) after a rejection, or a bonus drawn from
 // p_{k+1} when all k were accepted.  This is the modified rejection sampling
 // that makes the accepted tokens follow the target's distribution (paper
-// Sec. 1, Sec. 7; Table 1's caption: 1..k+1 tokens per round).
+// Sec. 1, Sec. 6; Table 1's caption: 1..k+1 tokens per round).
 //
 // Every decision is exact, so any order of evaluation gives the same tokens:
 //   * accept test r * q < p in fp64 (the product of two fp32 numbers is exact);

@@ -12,7 +12,7 @@ Paper Sec. 2 (evaluation metric):
     being the hardware operational intensity in FLOPs per byte;
   * hence dt = [k * max(C_d, (N_d + KV_d) HOI) + max((k+1) C_t, (N_t + KV_t) HOI)]
                / max(C_t, (N_t + KV_t) HOI).
-Paper Sec. 6 (cost analysis): with U units spent on decoding, drafting with a
+Paper Sec. 5 (cost analysis): with U units spent on decoding, drafting with a
 multiplier m saves U * (1 - 1/m) units; the draft's training cost is
 subtracted from that saving.
 
@@ -62,8 +62,14 @@ def throughput_multiplier(tau: float, dt: float) -> float:
     return tau / dt
 
 
+def implied_dt(tau: float, multiplier: float) -> float:
+    """The iteration time multiplier a printed throughput multiplier implies
+    for a measured tau (Sec. 2: multiplier = tau / dt)."""
+    return tau / multiplier
+
+
 def decode_cost_saved(units: float, multiplier: float) -> float:
-    """Decoding cost saved out of `units` by a throughput multiplier (Sec. 6)."""
+    """Decoding cost saved out of `units` by a throughput multiplier (Sec. 5)."""
     return units * (1.0 - 1.0 / multiplier)
 
 

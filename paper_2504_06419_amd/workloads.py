@@ -140,13 +140,13 @@ def named_workloads():
                             ctx_lo=2048, ctx_hi=65536, kv_dtype="fp8"),
             verify=VerifySpec(B=512, Hq=64, Hkv=8, D=128, k=8, ctx_lo=2048, ctx_hi=65536,
                               kv_dtype="fp8", page_size=16, spare_pages=64)),
-        # the vocabulary of Llama 3 (the model the paper extrapolates to, Sec. 5.3)
+        # the vocabulary of Llama 3 (the model the paper extrapolates to, Sec. 4.3)
         "token_verify_B256_k4_V128256": dict(token=TokenSpec(B=256, k=4, V=128256)),
         "token_verify_B512_k8_V128256": dict(token=TokenSpec(B=512, k=8, V=128256)),
         "kv_update_round_fp8_B512_k8": dict(kvupd=KvUpdateSpec(B=512, Hkv=8, D=128, k=8, S=4, W=4096,
                                                                 ctx_lo=2048, ctx_hi=65536)),
         # SPIRe's two-layer draft (embedding + 2 layers mixed into 2 memory
-        # vectors) at the width of Llama 3 70B, the model of Sec. 5.3
+        # vectors) at the width of Llama 3 70B, the model of Sec. 4.3
         "feedback_memory_B512_d8192": dict(fm=FeedbackSpec(B=512, d=8192, layers=3, n_out=2)),
         # one GPU's share of the fp8 round's verification under tensor
         # parallelism over the 8 KV heads: 8 query heads reading 1 KV head

@@ -10,6 +10,14 @@ if ROOT not in sys.path:
 
 def pytest_configure(config):
     config.addinivalue_line("markers", "gpu: needs an MI355X (gfx950) GPU and the built HIP library")
+    # another build of the same sources, e.g. the sanitizer builds that
+    # tests/test_sanitizers.py makes (test runs only)
+    if os.environ.get("SPIRE_TEST_LIB"):
+        from paper_2504_06419_amd import spire
+        spire.LIB_PATH = os.environ["SPIRE_TEST_LIB"]
+    if os.environ.get("SPIRE_TEST_ORACLE_LIB"):
+        from oracle import oracle as O
+        O.LIB = os.environ["SPIRE_TEST_ORACLE_LIB"]
 
 
 def pytest_collection_modifyitems(config, items):

@@ -1,6 +1,6 @@
 """Pins of the token verification oracle (CPU only).
 
-The oracle restates modified rejection sampling (paper Sec. 1 and Sec. 7; the
+The oracle restates modified rejection sampling (paper Sec. 1 and Sec. 6; the
 published scheme of Leviathan et al. 2023 / Chen et al. 2023).  It is pinned
 here by what the mathematics fixes, not by itself:
   * the guarantee the paper relies on: the first emitted token of a round is
