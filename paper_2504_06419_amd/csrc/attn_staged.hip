@@ -50,6 +50,16 @@ __device__ __forceinline__ void ring_barrier() {
     asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
+// One 16-byte DMA from a uniform base plus a 32-bit lane offset.  The empty
+// asm keeps the offset a 32-bit value at the load (otherwise the compiler
+// hoists its widening out of the tile loop, keeps 64-bit offsets in spare
+// registers and adds them with vector instructions), so the load takes the
+// form with a scalar base and a 32-bit vector offset.
+__device__ __forceinline__ void dma16_off(const uint8_t *base, uint32_t off, lds_u8 *l) {
+    asm volatile("" : "+v"(off));
+    dma16(base + off, l);
+}
+
 // Copy the K (PART & 1) and/or V (PART & 2) half of tile `tile` into `st`.
 template <bool FP8, int MODE, int PART>
 __device__ __forceinline__ void issue_tile(lds_u8 *st, const SegAddr &a, int tile, int lane) {
@@ -65,10 +75,13 @@ __device__ __forceinline__ void issue_tile(lds_u8 *st, const SegAddr &a, int til
 #pragma unroll
         for (int x = 0; x < G::KLOADS; ++x) {
             const int mb = x / NK, c = x % NK;
+            if (fast) {  // uniform group base + 32-bit lane offset (the host bounds 16 rows below 2^31 bytes)
+                dma16_off(a.kseq + (mb ? g1 : g0), (uint32_t)rho * (uint32_t)a.tok_bytes + (uint32_t)(64 * c + 16 * j),
+                          st + x * 1024);
+                continue;
+            }
             const uint8_t *row;
-            if (fast) {
-                row = a.kseq + (mb ? g1 : g0) + (int64_t)rho * a.tok_bytes;
-            } else if (MODE == MODE_DRAFT) {
+            if (MODE == MODE_DRAFT) {
                 row = draft_row(a, key0 + 16 * mb + rho, false);
             } else {
                 row = a.kseq + (int64_t)min(key0 + 16 * mb + rho, a.cap - 1) * a.tok_bytes;
@@ -84,10 +97,13 @@ __device__ __forceinline__ void issue_tile(lds_u8 *st, const SegAddr &a, int til
             // group: the transposing reads of 16 lanes then hit distinct banks)
             const int kin = FP8 ? 8 * x + (lane >> 3) : 4 * x + j;
             const int byte = FP8 ? 16 * (((lane & 7) - (kin >> 2)) & 7) : 16 * n16;
-            const uint8_t *row;
             if (fast) {
-                row = a.vseq + (kin < 16 ? g0 : g1) + (int64_t)(kin & 15) * a.tok_bytes;
-            } else if (MODE == MODE_DRAFT) {
+                dma16_off(a.vseq + (kin < 16 ? g0 : g1), (uint32_t)(kin & 15) * (uint32_t)a.tok_bytes + (uint32_t)byte,
+                          st + G::KBYTES + x * 1024);
+                continue;
+            }
+            const uint8_t *row;
+            if (MODE == MODE_DRAFT) {
                 row = draft_row(a, key0 + kin, true);
             } else {
                 row = a.vseq + (int64_t)min(key0 + kin, a.cap - 1) * a.tok_bytes;

@@ -436,11 +436,15 @@ static spire_status verify_impl(const void *q, int32_t q_dtype, const spire_kv *
     // paged: 16-key groups never straddle a page, and the matrix-core kernels
     // form page offsets with 32-bit products
     const int es = elem_size(kv->dtype);
+    // paged: 16-key groups never straddle a page, and the matrix-core kernels
+    // form page offsets with 32-bit products; both layouts: 16 key rows span
+    // under 2^31 bytes (32-bit lane offsets of the loads)
     const bool layout_ok =
-        kv->page_size > 0
-            ? (kv->page_size % 16 == 0 && (uint64_t)kv->s_blk * es < (1ull << 32) &&
-               (uint64_t)kv->page_size * kv->s_tok * es < (1ull << 31))
-            : (kv->capacity >= 1);
+        (uint64_t)kv->s_tok * es * 16 < (1ull << 31) &&
+        (kv->page_size > 0
+             ? (kv->page_size % 16 == 0 && (uint64_t)kv->s_blk * es < (1ull << 32) &&
+                (uint64_t)kv->page_size * kv->s_tok * es < (1ull << 31))
+             : (kv->capacity >= 1));
     const bool mfma = (kv->dtype == SPIRE_BF16 || kv->dtype == SPIRE_FP8_E4M3FN) &&
                       q_dtype == SPIRE_BF16 && D == 128 && p.R <= kMaxRows && layout_ok && rows_aligned(kv);
     return run(p, mfma, workspace, workspace_bytes, stream, KID_VERIFY, opts, lib_scratch);
@@ -505,8 +509,10 @@ spire_status spire_draft_sparse_attn_ex(const void *q, int32_t q_dtype, const sp
 
     const bool same_scales = ring->dtype != SPIRE_FP8_E4M3FN ||
                              (ring->k_scale == sink->k_scale && ring->v_scale == sink->v_scale);
+    // 16 ring rows span under 2^31 bytes (32-bit lane offsets of the loads)
     const bool mfma = (ring->dtype == SPIRE_BF16 || ring->dtype == SPIRE_FP8_E4M3FN) &&
                       q_dtype == SPIRE_BF16 && D == 128 && p.R <= kMaxRows && same_scales &&
+                      (uint64_t)ring->s_tok * elem_size(ring->dtype) * 16 < (1ull << 31) &&
                       rows_aligned(ring) && rows_aligned(sink);
     return run(p, mfma, workspace, workspace_bytes, stream, KID_DRAFT, opts);
 }
