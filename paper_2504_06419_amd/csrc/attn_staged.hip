@@ -15,9 +15,9 @@
 //     converts each tile once (two waves would both convert it) and needs no
 //     workgroup barrier; measured 3 % faster than 3 + 2 blocks on two waves.
 //
-// Stage layout (one 32-key tile): the K part is written in MFMA operand order
-// (DMA instruction x, lane L -> the 16 bytes lane L feeds to MFMA call x), so
-// every lane reads back its own slots; the V part is row-major (bf16: DMA lane
+// Stage layout (one 32-key tile): the K part is row-major with each row's
+// 16-byte chunks permuted (kswz: whole rows per copy instruction, reads free
+// of bank conflicts); the V part is row-major (bf16: DMA lane
 // L of instruction t = the 16 bytes of key 4t + L/16 lane L needs; fp8: 8 whole
 // 128-byte rows per instruction, each row's 16-byte chunks rotated by its key
 // group, read back transposed as the V^T operands: no byte permutes, measured
@@ -60,33 +60,46 @@ __device__ __forceinline__ void dma16_off(const uint8_t *base, uint32_t off, lds
     dma16(base + off, l);
 }
 
+// K stage layout: row-major, key row r of the tile at r * RB bytes (RB = 128
+// fp8, 256 bf16), its 16-byte chunk q at position q ^ kswz(r): each copy
+// instruction moves whole rows (8 fp8 / 4 bf16 rows of 1 KB, every 128-byte
+// line in one request), and the MFMA-operand reads -- 16 lanes, one per row,
+// the same chunk -- still land on distinct banks, with 128 or with 256 bytes
+// of banks per cycle.
+template <bool FP8> __device__ __forceinline__ int kswz(int r) {
+    r &= 15;
+    if constexpr (FP8) return ((r >> 2) & 3) | (((r ^ (r >> 1)) & 1) << 2);
+    return 4 * (r & 3) + (r >> 2);
+}
+
 // Copy the K (PART & 1) and/or V (PART & 2) half of tile `tile` into `st`.
 template <bool FP8, int MODE, int PART>
 __device__ __forceinline__ void issue_tile(lds_u8 *st, const SegAddr &a, int tile, int lane) {
     using G = Stage<FP8>;
     const int n16 = lane & 15, j = lane >> 4;
-    const int rho = 4 * (n16 & 3) + (n16 >> 2);
     const int key0 = tile * kMfmaTile;
     const int64_t g0 = group_base<MODE>(a, key0);
     const int64_t g1 = group_base<MODE>(a, key0 + 16);
     const bool fast = MODE == MODE_PAGED || (g0 >= 0 && g1 >= 0);
     if (PART & 1) {
-        constexpr int NK = FP8 ? 2 : 4;  // 16-byte chunks per key row per lane
+        constexpr int CPR = FP8 ? 8 : 16;   // 16-byte chunks per key row
+        constexpr int RPI = 64 / CPR;       // rows per copy instruction
 #pragma unroll
         for (int x = 0; x < G::KLOADS; ++x) {
-            const int mb = x / NK, c = x % NK;
+            const int r = RPI * x + lane / CPR;
+            const int q = (lane % CPR) ^ kswz<FP8>(r);
             if (fast) {  // uniform group base + 32-bit lane offset (the host bounds 16 rows below 2^31 bytes)
-                dma16_off(a.kseq + (mb ? g1 : g0), (uint32_t)rho * (uint32_t)a.tok_bytes + (uint32_t)(64 * c + 16 * j),
-                          st + x * 1024);
+                dma16_off(a.kseq + (x < G::KLOADS / 2 ? g0 : g1),
+                          (uint32_t)(r & 15) * (uint32_t)a.tok_bytes + (uint32_t)(16 * q), st + x * 1024);
                 continue;
             }
             const uint8_t *row;
             if (MODE == MODE_DRAFT) {
-                row = draft_row(a, key0 + 16 * mb + rho, false);
+                row = draft_row(a, key0 + r, false);
             } else {
-                row = a.kseq + (int64_t)min(key0 + 16 * mb + rho, a.cap - 1) * a.tok_bytes;
+                row = a.kseq + (int64_t)min(key0 + r, a.cap - 1) * a.tok_bytes;
             }
-            dma16(row + 64 * c + 16 * j, st + x * 1024);
+            dma16(row + 16 * q, st + x * 1024);
         }
     }
     if (PART & 2) {
@@ -117,11 +130,17 @@ template <bool FP8>
 __device__ __forceinline__ void read_tile(TileRegs<FP8> &T, const lds_u8 *st, int lane) {
     using G = Stage<FP8>;
     const int n16 = lane & 15, j = lane >> 4;
+    // MFMA operand (mb, c) of this lane: key row 16 mb + rho, chunk 4 c + j
     constexpr int NK = FP8 ? 2 : 4;
+    constexpr int RB = FP8 ? 128 : 256;
+    const int rho = 4 * (n16 & 3) + (n16 >> 2);
+    const int sw = kswz<FP8>(rho);
 #pragma unroll
-    for (int x = 0; x < G::KLOADS; ++x)
-        T.k[x / NK][x % NK] = *reinterpret_cast<const __attribute__((address_space(3))) u32x4 *>(
-            st + x * 1024 + lane * 16);
+    for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+        for (int c = 0; c < NK; ++c)
+            T.k[mb][c] = *reinterpret_cast<const __attribute__((address_space(3))) u32x4 *>(
+                st + (16 * mb + rho) * RB + 16 * ((4 * c + j) ^ sw));
     if constexpr (FP8) {
         // Transposing reads (ds_read_b64_tr_b8): byte t of lane i of a 16-lane
         // group is byte i % 8 of the 8 bytes lane 2t + i/8 of the group
