@@ -560,22 +560,31 @@ FLUSH_BYTES = 512 << 20
 
 def timed_steps(step, steps: int, flush: bool) -> list:
     """Time `steps` steps between two events each on the launch stream, after
-    a synchronisation on both sides of the region.  With `flush`, a 512 MiB
-    scratch write before every step (outside its events) evicts the L2s and the
-    256 MB Infinity Cache, so every step reads its K/V from HBM.  Returns the
+    a synchronisation on both sides of the region.  With `flush`, before every
+    step (outside its events) a 512 MiB scratch buffer is written, which evicts
+    the L2s and the 256 MB Infinity Cache, and then a second 512 MiB buffer is
+    read with ordinary loads, which replaces the written lines with clean ones:
+    every step then reads its K/V from HBM and pays no write-back of the
+    flush's own data (measured on the 256-sequence workload: write-only flush
+    2.362 ms per step, write + read 2.322 ms, no flush 2.316 ms).  Returns the
     per-step times in ms."""
     st = torch.cuda.current_stream()
-    scratch = torch.empty((FLUSH_BYTES,), dtype=torch.uint8, device="cuda") if flush else None
+    if flush:
+        dirty = torch.empty((FLUSH_BYTES,), dtype=torch.uint8, device="cuda")
+        clean = torch.ones((FLUSH_BYTES // 4,), dtype=torch.int32, device="cuda")
+        total = torch.empty((), dtype=torch.int64, device="cuda")
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
     torch.cuda.synchronize()
     for i in range(steps):
         if flush:
-            scratch.fill_(i & 0xFF)
+            dirty.fill_(i & 0xFF)
+            torch.sum(clean, dim=0, out=total)
         ev[i][0].record(st)
         step()
         ev[i][1].record(st)
     torch.cuda.synchronize()
-    del scratch
+    if flush:
+        del dirty, clean, total
     return [a.elapsed_time(b) for a, b in ev]
 
 
