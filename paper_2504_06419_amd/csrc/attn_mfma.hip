@@ -91,17 +91,19 @@ __global__ __launch_bounds__(256, 1) void mfma_partial_kernel(Problem p, Plan pl
         if (n > 0) {
             const int last = t1 - 1;
             TileRegs<FP8> A, Bt, C;  // three register buffers, two tiles in flight
+            // only tiles of the range are loaded (a buffer is computed only
+            // after its load)
             load_tile<FP8, MODE>(A, a, tile, lane);
-            load_tile<FP8, MODE>(Bt, a, tile + 1 < last ? tile + 1 : last, lane);
+            if (tile + 1 <= last) load_tile<FP8, MODE>(Bt, a, tile + 1, lane);
             int tt = tile;
             while (true) {
-                load_tile<FP8, MODE>(C, a, tt + 2 < last ? tt + 2 : last, lane);
+                if (tt + 2 <= last) load_tile<FP8, MODE>(C, a, tt + 2, lane);
                 compute_tile<FP8, NB>(A, qf, st, tt, n, full_lim, sc, lane);
                 if (++tt > last) break;
-                load_tile<FP8, MODE>(A, a, tt + 2 < last ? tt + 2 : last, lane);
+                if (tt + 2 <= last) load_tile<FP8, MODE>(A, a, tt + 2, lane);
                 compute_tile<FP8, NB>(Bt, qf, st, tt, n, full_lim, sc, lane);
                 if (++tt > last) break;
-                load_tile<FP8, MODE>(Bt, a, tt + 2 < last ? tt + 2 : last, lane);
+                if (tt + 2 <= last) load_tile<FP8, MODE>(Bt, a, tt + 2, lane);
                 compute_tile<FP8, NB>(C, qf, st, tt, n, full_lim, sc, lane);
                 if (++tt > last) break;
             }
