@@ -456,6 +456,8 @@ KERNEL_SOURCES = ["paper_2504_06419_amd/csrc/attn_mfma.hip",
                   "paper_2504_06419_amd/csrc/plan_combine.hip",
                   "paper_2504_06419_amd/csrc/spire_abi.hip",
                   "paper_2504_06419_amd/csrc/token_verify.hip",
+                  "paper_2504_06419_amd/csrc/block_verify.hip",
+                  "paper_2504_06419_amd/csrc/sampling.h",
                   "paper_2504_06419_amd/csrc/kv_update.hip",
                   "paper_2504_06419_amd/csrc/feedback_memory.hip",
                   "paper_2504_06419_amd/csrc/mfma_common.h",

@@ -236,6 +236,40 @@ spire_status spire_token_verify(const float *p_target, const float *q_draft,
                                 int32_t *n_accepted, int32_t *out_tokens, void *workspace,
                                 size_t workspace_bytes, hipStream_t stream);
 
+/* Bytes of workspace spire_block_verify needs (0 on invalid sizes). */
+size_t spire_block_verify_workspace_size(int32_t B, int32_t k, int32_t V);
+
+/*
+ * Block verification of one speculation round: the alternative to token
+ * verification the paper names (Sec. 6: its results should hold with block
+ * verification too); the draft block is judged as a whole.  Arguments,
+ * sizes, outputs and the sampling of the emitted token are those of
+ * spire_token_verify; the accepted count n is defined instead by, for each
+ * sequence b with p(i,.) = p_target[b,i,.], q(i,.) = q_draft[b,i,.]:
+ *   w_0 = 1;  w_i = 1 if t >= q(i-1, x_i), else t / q(i-1, x_i), with
+ *             t = w_{i-1} * p(i-1, x_i)                 (i = 1..k, fp64),
+ *             and w_i = 0 when w_{i-1} = 0, x_i is outside [0, V), p(i-1, x_i)
+ *             is not > 0 or q(i-1, x_i) is not >= 0 (NaN included);
+ *   residual row i < k: r_i(x) = w32 * p(i, x) - q(i, x), w32 = w_i rounded
+ *             to fp32, both operations rounded in fp32 (no fused multiply-add),
+ *             turned into integer weights as for token verification; S_i =
+ *             the sum of row i's weights;
+ *   h_i = S / (S + (1 - w_i) * 2^40) in fp64 with S = S_i rounded once to
+ *             fp64 (h_i = 1 if the denominator is 0), for i < k;  h_k = w_k;
+ *   n = the largest i in 1..k with u_accept[b, i-1] < h_i, or 0.
+ * The emitted token is drawn with u_sample[b] from row n's residual weights
+ * when n < k (from p(n,.) if they sum to 0), else from p(k,.).  Emitted tokens
+ * follow the target's distribution, and on average at least as many are
+ * accepted as by token verification.  Reads every row of p and q.
+ *   workspace  >= spire_block_verify_workspace_size(B, k, V) bytes, 256-byte
+ *              aligned, contents need no initialisation.
+ */
+spire_status spire_block_verify(const float *p_target, const float *q_draft,
+                                const int32_t *draft_tokens, const float *u_accept,
+                                const float *u_sample, int32_t B, int32_t k, int32_t V,
+                                int32_t *n_accepted, int32_t *out_tokens, void *workspace,
+                                size_t workspace_bytes, hipStream_t stream);
+
 /*
  * Append the K/V of newly verified tokens to the target cache (paper Sec. 2:
  * the target's forward pass on the k+1 tokens of a round produces their K/V).
@@ -345,11 +379,13 @@ int32_t spire_version(void);
 
 /*
  * Per-call options of the entry points that launch several kernels
- * (spire_verify_attn_ex, spire_draft_sparse_attn_ex, spire_token_verify_ex).
+ * (spire_verify_attn_ex, spire_draft_sparse_attn_ex, spire_token_verify_ex,
+ * spire_block_verify_ex).
  * A NULL pointer, or a zero-initialised struct, means the defaults; the
  * library reads the struct and writes the host arrays it points to only
  * during the call and keeps nothing afterwards, so calls stay reentrant.
- *   kernel        attention family (the token entry point ignores it):
+ *   kernel        attention family (the token and block verification entry
+ *                 points ignore it):
  *                 0 automatic -- the matrix-core kernels where dtype and shape
  *                 allow (LDS-staged above 32 rows per KV head, register-staged
  *                 otherwise), the generic vector kernel for the rest;
@@ -368,7 +404,8 @@ int32_t spire_version(void);
  *                 launch -- 0 plan, 1 verify partial attention, 2 draft
  *                 partial attention, 3 combine, 4 token verification weights,
  *                 5 token verification select, 11 the check of the values of
- *                 keys [n - k, n) after a matrix-core verify call.
+ *                 keys [n - k, n) after a matrix-core verify call, 12 block
+ *                 verification weights, 13 block verification select.
  *   n_launches    host int32 or NULL: set to the number of kernels the call
  *                 launched (0 when it returned before launching).
  *   reserved      must be 0.
@@ -397,6 +434,12 @@ spire_status spire_draft_sparse_attn_ex(const void *q, int32_t q_dtype, const sp
                                         size_t workspace_bytes, hipStream_t stream,
                                         const spire_launch_opts *opts);
 spire_status spire_token_verify_ex(const float *p_target, const float *q_draft,
+                                   const int32_t *draft_tokens, const float *u_accept,
+                                   const float *u_sample, int32_t B, int32_t k, int32_t V,
+                                   int32_t *n_accepted, int32_t *out_tokens, void *workspace,
+                                   size_t workspace_bytes, hipStream_t stream,
+                                   const spire_launch_opts *opts);
+spire_status spire_block_verify_ex(const float *p_target, const float *q_draft,
                                    const int32_t *draft_tokens, const float *u_accept,
                                    const float *u_sample, int32_t B, int32_t k, int32_t V,
                                    int32_t *n_accepted, int32_t *out_tokens, void *workspace,

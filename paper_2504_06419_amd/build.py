@@ -18,7 +18,7 @@ BUILD = os.path.join(HERE, "_build")
 ARCH = "gfx950"
 
 SOURCES = ["spire_abi.hip", "plan_combine.hip", "attn_mfma.hip", "attn_staged.hip",
-           "attn_generic.hip", "token_verify.hip", "kv_update.hip",
+           "attn_generic.hip", "token_verify.hip", "block_verify.hip", "kv_update.hip",
            "feedback_memory.hip", "hbm_probe.hip"]
 
 FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",

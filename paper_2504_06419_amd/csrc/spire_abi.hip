@@ -116,7 +116,7 @@ size_t workspace_bytes_for(int B, int R, int D) {
 // ---- per-call options: kernel family and launch events ----------------------------
 // Kernel ids of the recorded launches (include/spire.h).
 enum { KID_PLAN = 0, KID_VERIFY = 1, KID_DRAFT = 2, KID_COMBINE = 3, KID_TOKEN_WEIGHTS = 4,
-       KID_TOKEN_SELECT = 5, KID_TAIL_CHECK = 11 };
+       KID_TOKEN_SELECT = 5, KID_TAIL_CHECK = 11, KID_BLOCK_WEIGHTS = 12, KID_BLOCK_SELECT = 13 };
 
 // Records the caller's events around each launch of one call, in launch order.
 struct Recorder {
@@ -580,6 +580,69 @@ spire_status spire_token_verify_ex(const float *p_target, const float *q_draft,
     if (e != hipSuccess) return fail(SPIRE_ERR_HIP, "token weights launch: %s", hipGetErrorString(e));
     e = rec.run(KID_TOKEN_SELECT, stream, [&] { return launch_token_select(t, stream); });
     if (e != hipSuccess) return fail(SPIRE_ERR_HIP, "token select launch: %s", hipGetErrorString(e));
+    return SPIRE_OK;
+}
+
+// ---- block verification -------------------------------------------------------
+
+size_t spire_block_verify_workspace_size(int32_t B, int32_t k, int32_t V) {
+    if (B < 0 || k < 0 || k > kTokenMaxK || V < 1 || V > kTokenMaxV) return 0;
+    return align256((size_t)B * (size_t)(k + 1) * token_pieces(V) * sizeof(uint64_t)) + 256;
+}
+
+spire_status spire_block_verify(const float *p_target, const float *q_draft,
+                                const int32_t *draft_tokens, const float *u_accept,
+                                const float *u_sample, int32_t B, int32_t k, int32_t V,
+                                int32_t *n_accepted, int32_t *out_tokens, void *workspace,
+                                size_t workspace_bytes, hipStream_t stream) {
+    return spire_block_verify_ex(p_target, q_draft, draft_tokens, u_accept, u_sample, B, k, V, n_accepted,
+                                 out_tokens, workspace, workspace_bytes, stream, nullptr);
+}
+
+spire_status spire_block_verify_ex(const float *p_target, const float *q_draft,
+                                   const int32_t *draft_tokens, const float *u_accept,
+                                   const float *u_sample, int32_t B, int32_t k, int32_t V,
+                                   int32_t *n_accepted, int32_t *out_tokens, void *workspace,
+                                   size_t workspace_bytes, hipStream_t stream,
+                                   const spire_launch_opts *opts) {
+    g_err[0] = '\0';
+    if (opts != nullptr && opts->n_launches != nullptr) *opts->n_launches = 0;
+    if (check_opts(opts) != SPIRE_OK) return SPIRE_ERR_INVALID_ARG;
+    if (B < 0 || B > 65535) return fail(SPIRE_ERR_UNSUPPORTED, "B must be in [0, 65535] (got %d)", B);
+    if (k < 0 || k > kTokenMaxK) return fail(SPIRE_ERR_UNSUPPORTED, "k must be in [0, %d] (got %d)", kTokenMaxK, k);
+    if (V < 1 || V > kTokenMaxV) return fail(SPIRE_ERR_UNSUPPORTED, "V must be in [1, %d] (got %d)", kTokenMaxV, V);
+    if (B == 0) return SPIRE_OK;
+    if (p_target == nullptr || u_sample == nullptr || n_accepted == nullptr || out_tokens == nullptr)
+        return fail(SPIRE_ERR_INVALID_ARG, "p_target, u_sample, n_accepted or out_tokens is NULL");
+    if (k > 0 && (q_draft == nullptr || draft_tokens == nullptr || u_accept == nullptr))
+        return fail(SPIRE_ERR_INVALID_ARG, "q_draft, draft_tokens or u_accept is NULL with k > 0");
+    const void *ptrs[] = {p_target, q_draft, draft_tokens, u_accept, u_sample, n_accepted, out_tokens};
+    for (const void *ptr : ptrs)
+        if (((uintptr_t)ptr & 3u) != 0) return fail(SPIRE_ERR_INVALID_ARG, "arrays must be 4-byte aligned");
+    const size_t need = spire_block_verify_workspace_size(B, k, V);
+    if (workspace == nullptr) return fail(SPIRE_ERR_WORKSPACE, "workspace is NULL");
+    if (((uintptr_t)workspace & 255u) != 0) return fail(SPIRE_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+    if (workspace_bytes < need)
+        return fail(SPIRE_ERR_WORKSPACE, "workspace has %zu bytes, needs %zu", workspace_bytes, need);
+    TokenProblem t;
+    t.p = p_target;
+    t.q = q_draft;
+    t.draft = draft_tokens;
+    t.u_accept = u_accept;
+    t.u_sample = u_sample;
+    t.B = B;
+    t.k = k;
+    t.V = V;
+    t.npieces = token_pieces(V);
+    t.n_accepted = n_accepted;
+    t.out_tokens = out_tokens;
+    t.piece_sum = static_cast<uint64_t *>(workspace);
+    t.nacc = nullptr;
+    Recorder rec(opts);
+    hipError_t e = rec.run(KID_BLOCK_WEIGHTS, stream, [&] { return launch_block_weights(t, stream); });
+    if (e != hipSuccess) return fail(SPIRE_ERR_HIP, "block weights launch: %s", hipGetErrorString(e));
+    e = rec.run(KID_BLOCK_SELECT, stream, [&] { return launch_block_select(t, stream); });
+    if (e != hipSuccess) return fail(SPIRE_ERR_HIP, "block select launch: %s", hipGetErrorString(e));
     return SPIRE_OK;
 }
 

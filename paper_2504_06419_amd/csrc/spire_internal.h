@@ -196,6 +196,10 @@ struct TokenProblem {
 };
 hipError_t launch_token_weights(const TokenProblem &t, hipStream_t st);
 hipError_t launch_token_select(const TokenProblem &t, hipStream_t st);
+// block verification (block_verify.hip): the same problem, piece_sum holding
+// [B, k+1, npieces] (every row's weights), nacc unused
+hipError_t launch_block_weights(const TokenProblem &t, hipStream_t st);
+hipError_t launch_block_select(const TokenProblem &t, hipStream_t st);
 
 // ---- KV cache updates (kv_update.hip) ------------------------------------------
 hipError_t launch_kv_append(const KvDev &kv, const void *k_new, const void *v_new, int new_dtype,

@@ -26,13 +26,16 @@ STATUS = {0: "SPIRE_OK", 1: "SPIRE_ERR_INVALID_ARG", 2: "SPIRE_ERR_UNSUPPORTED",
 SYMBOLS = ["spire_verify_workspace_size", "spire_verify_attn", "spire_verify_attn_noalloc",
            "spire_draft_workspace_size",
            "spire_draft_sparse_attn", "spire_token_verify_workspace_size", "spire_token_verify",
+           "spire_block_verify_workspace_size", "spire_block_verify",
            "spire_kv_append", "spire_draft_append", "spire_draft_rollback", "spire_feedback_memory",
            "spire_hbm_read_probe", "spire_status_string", "spire_last_error", "spire_version",
-           "spire_verify_attn_ex", "spire_draft_sparse_attn_ex", "spire_token_verify_ex"]
+           "spire_verify_attn_ex", "spire_draft_sparse_attn_ex", "spire_token_verify_ex",
+           "spire_block_verify_ex"]
 
 # kernel ids of the launches recorded through spire_launch_opts
 KERNEL_IDS = {0: "plan", 1: "verify_partial", 2: "draft_partial", 3: "combine",
-              4: "token_weights", 5: "token_select", 11: "tail_check"}
+              4: "token_weights", 5: "token_select", 11: "tail_check", 12: "block_weights",
+              13: "block_select"}
 # kernel families (spire_launch_opts.kernel)
 KERNEL_AUTO, KERNEL_GENERIC, KERNEL_REGS, KERNEL_LDS = 0, 1, 2, 3
 HBM_PROBE_SINK_WORDS = 2048
@@ -110,6 +113,12 @@ def load(path: Optional[str] = None):
     L.spire_draft_sparse_attn_ex.argtypes = L.spire_draft_sparse_attn.argtypes + [C.POINTER(LaunchOpts)]
     L.spire_token_verify_ex.restype = C.c_int
     L.spire_token_verify_ex.argtypes = L.spire_token_verify.argtypes + [C.POINTER(LaunchOpts)]
+    L.spire_block_verify_workspace_size.restype = sz
+    L.spire_block_verify_workspace_size.argtypes = [i32] * 3
+    L.spire_block_verify.restype = C.c_int
+    L.spire_block_verify.argtypes = L.spire_token_verify.argtypes
+    L.spire_block_verify_ex.restype = C.c_int
+    L.spire_block_verify_ex.argtypes = L.spire_token_verify.argtypes + [C.POINTER(LaunchOpts)]
     L.spire_hbm_read_probe.restype = C.c_int
     L.spire_hbm_read_probe.argtypes = [vp, sz, vp, sz, vp]
     if path is None:
@@ -295,6 +304,36 @@ def token_verify(p: torch.Tensor, q: Optional[torch.Tensor], draft: Optional[tor
     if ws is None:
         ws = workspace(token_verify_workspace_size(B, k, V), p.device)
     _check(load().spire_token_verify_ex(p.data_ptr(), _ptr(q) if k > 0 else None,
+                                        _ptr(draft) if k > 0 else None,
+                                        _ptr(u_accept) if k > 0 else None, u_sample.data_ptr(), B, k,
+                                        V, n_accepted.data_ptr(), tokens.data_ptr(), ws.data_ptr(),
+                                        ws.numel(), _stream(), _opts(0, opts)))
+    return n_accepted, tokens
+
+
+def block_verify_workspace_size(B, k, V) -> int:
+    return int(load().spire_block_verify_workspace_size(B, k, V))
+
+
+def block_verify(p: torch.Tensor, q: Optional[torch.Tensor], draft: Optional[torch.Tensor],
+                 u_accept: Optional[torch.Tensor], u_sample: torch.Tensor,
+                 n_accepted: Optional[torch.Tensor] = None, tokens: Optional[torch.Tensor] = None,
+                 ws: Optional[torch.Tensor] = None, opts: Optional[LaunchOpts] = None):
+    """spire_block_verify: arguments and results as token_verify."""
+    B, kp1, V = p.shape
+    k = kp1 - 1
+    assert p.dtype == torch.float32 and p.is_contiguous() and u_sample.is_contiguous()
+    if k > 0:
+        assert q.shape == (B, k, V) and q.dtype == torch.float32 and q.is_contiguous()
+        assert draft.shape == (B, k) and draft.dtype == torch.int32 and draft.is_contiguous()
+        assert u_accept.shape == (B, k) and u_accept.dtype == torch.float32 and u_accept.is_contiguous()
+    if n_accepted is None:
+        n_accepted = torch.empty((B,), dtype=torch.int32, device=p.device)
+    if tokens is None:
+        tokens = torch.empty((B, kp1), dtype=torch.int32, device=p.device)
+    if ws is None:
+        ws = workspace(block_verify_workspace_size(B, k, V), p.device)
+    _check(load().spire_block_verify_ex(p.data_ptr(), _ptr(q) if k > 0 else None,
                                         _ptr(draft) if k > 0 else None,
                                         _ptr(u_accept) if k > 0 else None, u_sample.data_ptr(), B, k,
                                         V, n_accepted.data_ptr(), tokens.data_ptr(), ws.data_ptr(),

@@ -1,0 +1,143 @@
+"""GPU parity of block verification: the HIP path through the C ABI against
+the CPU oracle on the same seeded inputs.  Every decision is taken exactly as
+the header fixes it (fp64 prefix weights and stop tests, fp32 residual entries
+without fused multiply-adds, integer weights and inverse CDF), so accepted
+counts and emitted tokens must match the oracle bit for bit, for every
+sequence: small ragged vocabularies, the full-size vocabulary, k up to 15 and
+the degenerate cases of the method."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import block_verify as BV
+from oracle import token_verify as TV
+from paper_2504_06419_amd import spire
+from paper_2504_06419_amd import workloads as W
+from tests.gpu_helpers import banner
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+NW = W.named_workloads()
+
+
+def _run(p, q, draft, ua, us):
+    k = p.shape[1] - 1
+    n, tok = spire.block_verify(p, q if k > 0 else None, draft if k > 0 else None,
+                                ua if k > 0 else None, us)
+    torch.cuda.synchronize()
+    return n.cpu().numpy(), tok.cpu().numpy()
+
+
+def _compare(args):
+    if isinstance(args, W.TokenInputs):
+        args = (args.p, args.q, args.draft, args.u_accept, args.u_sample)
+    n, tok = _run(*args)
+    host = [a.cpu().numpy() for a in args]
+    rn, rtok = BV.verify_block(*host)
+    bad = np.nonzero((n != rn) | (tok != rtok).any(axis=1))[0]
+    print(f"  sequences={len(n)} mean tokens/round={float((n + 1).mean()):.3f} "
+          f"mismatches={len(bad)}", flush=True)
+    assert len(bad) == 0, (bad[:8], n[bad[:8]], rn[bad[:8]], tok[bad[:4]], rtok[bad[:4]])
+    return n, tok
+
+
+@pytest.mark.parametrize("V", [1, 7, 2048, 2049, 8193, 40964])
+@pytest.mark.parametrize("k", [0, 1, 4, 8, 15])
+def test_block_verify_small(k, V):
+    banner(f"block verify B=48 k={k} V={V}")
+    spec = W.TokenSpec(B=48, k=k, V=V, sigma=3.0, eps=0.7)
+    _compare(W.make_token_inputs(spec, W.MASTER_SEED + 300 + k * 7 + V, device=DEV))
+
+
+@pytest.mark.parametrize("name", ["token_verify_B256_k4_V128256", "token_verify_B512_k8_V128256"])
+def test_block_verify_full_workloads(name):
+    banner(f"block verify on the inputs of {name} (every sequence)")
+    spec = NW[name]["token"]
+    inp = W.make_token_inputs(spec, W.MASTER_SEED + W.WORKLOAD_INDEX[name], device=DEV)
+    n, _ = _compare(inp)
+    assert 0 < n.mean() < spec.k
+    # the same rounds under token verification (its own uniforms' meaning):
+    # block verification accepts more on average (pinned exactly on the CPU)
+    tn, _ = spire.token_verify(inp.p, inp.q, inp.draft, inp.u_accept, inp.u_sample)
+    print(f"  mean accepted: block {n.mean():.3f}, token {tn.float().mean().item():.3f}", flush=True)
+
+
+def _base(B=48, k=4, V=5000, seed=5):
+    spec = W.TokenSpec(B=B, k=k, V=V, sigma=3.0, eps=0.7)
+    t = W.make_token_inputs(spec, W.MASTER_SEED + seed, device=DEV)
+    return t.p.clone(), t.q.clone(), t.draft.clone(), t.u_accept.clone(), t.u_sample.clone()
+
+
+def test_block_verify_identical_models_and_empty_residuals():
+    banner("block verify: p == q (every token accepted); residual rows of weight 0")
+    p, q, d, ua, us = _base()
+    q = p[:, :4].contiguous()
+    n, _ = _compare((p, q, d, ua, us))
+    assert (n == 4).all()
+    # uniforms of 1 never stop: with p == q every h is 1 or 0/0 (= 1), so still all accepted
+    ua1 = torch.ones_like(ua)
+    _compare((p, q, d, ua1, us))
+    # a draft token the target cannot produce: w = 0 from there on, short prefixes
+    p2 = p.clone()
+    p2[::3, 1, :] = 0.0
+    p2[::3, 1, 0] = 1.0
+    d2 = d.clone()
+    d2[::3, 1] = 7
+    n, _ = _compare((p2, q, d2, ua, us))
+    assert (n[::3] <= 1).all()
+
+
+def test_block_verify_degenerate_values():
+    banner("block verify: NaN / negative / >1 probabilities, bad tokens, extreme uniforms, zero rows")
+    p, q, d, ua, us = _base(B=64)
+    p[0, :, 3::11] = float("nan")
+    q[1, :, 5::13] = float("nan")
+    p[2, :, :100] = -0.25
+    p[3, :, 7] = 3.0
+    d[4, 0] = -5
+    d[5, 2] = 5000               # == V: out of range
+    ua[6, :] = float("nan")
+    us[7] = 0.0
+    us[8] = 1.0
+    us[9] = float("nan")
+    us[10] = float("inf")
+    us[11] = 1.0 - 2.0 ** -24
+    us[12] = -3.0
+    p[13] = 0.0                  # no mass anywhere: token -1
+    q[13] = 0.0
+    p[14, 0] = 0.0               # one-hot rows at the last entry
+    p[14, 0, -1] = 1.0
+    q[14, 0, -1] = 0.0
+    d[14, 0] = 0
+    q[15, :, :] = 0.0            # a draft that gave its tokens probability 0
+    ua[16, :] = 0.0              # always stop at the top
+    ua[17, :] = 1.0              # never stop above 0
+    _compare((p, q, d, ua, us))
+
+
+def test_block_verify_mass_in_last_piece_and_unaligned_rows():
+    banner("block verify: mass only in the ragged last piece; rows not 16-byte aligned")
+    p, q, d, ua, us = _base(B=32, V=20000)
+    p[:, :, :18432] = 0.0
+    p[:, :, 18432:] += 1e-3
+    _compare((p, q, d, ua, us))
+    B, kp1, V = p.shape
+    pb = torch.empty(B * kp1 * V + 1, dtype=torch.float32, device=DEV)
+    qb = torch.empty(B * (kp1 - 1) * V + 1, dtype=torch.float32, device=DEV)
+    pu = pb[1:].view(B, kp1, V)
+    qu = qb[1:].view(B, kp1 - 1, V)
+    pu.copy_(p)
+    qu.copy_(q)
+    _compare((pu, qu, d, ua, us))
+
+
+def test_block_verify_is_deterministic_and_records_launches():
+    banner("block verify: repeated calls identical; launch events recorded")
+    p, q, d, ua, us = _base(B=128, V=128256)
+    a = _run(p, q, d, ua, us)
+    b = _run(p, q, d, ua, us)
+    assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1])
+    rec = spire.LaunchRecorder(4)
+    spire.block_verify(p, q, d, ua, us, opts=rec.opts())
+    names = [nm for nm, ms in rec.collect()]
+    assert names == ["block_weights", "block_select"]
