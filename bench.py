@@ -93,6 +93,8 @@ def build_workload(name: str, dev):
     v = W.make_verify_inputs(wl["verify"], seed, device=dev, poison=None) if "verify" in wl else None
     d = W.make_draft_inputs(wl["draft"], seed, device=dev, poison=None) if "draft" in wl else None
     t = W.make_token_inputs(wl["token"], seed, device=dev) if "token" in wl else None
+    if "block" in wl:
+        t = W.make_token_inputs(wl["block"], seed, device=dev)
     if "kvupd" in wl:
         t = W.make_kvupdate_inputs(wl["kvupd"], seed, device=dev)
     if "fm" in wl:
@@ -133,6 +135,36 @@ def make_token_step(t: W.TokenInputs):
     n = n_acc.cpu().tolist()
     emitted = sum(x + 1 for x in n)
     return step, step_recorded, token_bytes(t, n), emitted, emitted / s.B
+
+
+def block_bytes(t: W.TokenInputs) -> int:
+    """Algorithmic bytes of one block verification call: every row of p
+    (k+1) and of q (k) is read once (every row's residual mass enters the
+    accepted count), the k draft tokens with p and q at them, the uniforms,
+    and the outputs (n and k+1 tokens)."""
+    s = t.spec
+    return s.B * (4 * (2 * s.k + 1) * s.V + 16 * s.k + 4 * s.k + 4 + 4 * (s.k + 2))
+
+
+def make_block_step(t: W.TokenInputs):
+    """Return (step_fn, step_recorded_fn, bytes_per_step, emitted tokens per
+    step, mean tokens per round) of block verification."""
+    s = t.spec
+    ws = spire.workspace(spire.block_verify_workspace_size(s.B, s.k, s.V))
+    n_acc = torch.empty((s.B,), dtype=torch.int32, device=t.p.device)
+    toks = torch.empty((s.B, s.k + 1), dtype=torch.int32, device=t.p.device)
+    rec = spire.LaunchRecorder(4)
+
+    def step():
+        spire.block_verify(t.p, t.q, t.draft, t.u_accept, t.u_sample, n_acc, toks, ws)
+
+    def step_recorded():
+        spire.block_verify(t.p, t.q, t.draft, t.u_accept, t.u_sample, n_acc, toks, ws, opts=rec.opts())
+        return rec.collect()
+    step()
+    torch.cuda.synchronize()
+    emitted = int((n_acc + 1).sum().item())
+    return step, step_recorded, block_bytes(t), emitted, emitted / s.B
 
 
 def timed_call(name, fn):
@@ -287,7 +319,8 @@ def run_cpu_baseline_fm(x: W.FeedbackInputs, budget_s: float):
 
 
 def dominant_bytes(v, d, dominant, token_step_bytes=None):
-    if dominant in ("token_weights", "draft_append", "kv_append", "draft_rollback", "feedback_memory"):
+    if dominant in ("token_weights", "block_weights", "draft_append", "kv_append", "draft_rollback",
+                    "feedback_memory"):
         return token_step_bytes[dominant] if isinstance(token_step_bytes, dict) else token_step_bytes
     if dominant == "verify_partial":
         return verify_bytes(v)
@@ -341,6 +374,31 @@ def oracle_sample_draft(d, ids, step):
               for b in ids)
     nbytes = 2 * vis * s.Hkv * s.D * ELEM[s.kv_dtype] + len(ids) * s.Hq * s.D * (ELEM[s.q_dtype] + 4)
     return dt, nbytes, len(ids)
+
+
+def run_cpu_baseline_block(t: W.TokenInputs, budget_s: float):
+    """The block verification oracle (single-threaded Python + numpy) on whole
+    sequences of the same batch, a seeded order, until the time budget."""
+    from oracle import block_verify as BV
+    s = t.spec
+    g = torch.Generator().manual_seed(0)
+    order = torch.randperm(s.B, generator=g).tolist()
+    per_seq = block_bytes(t) / s.B
+    total_t, emitted, used, pos = 0.0, 0, 0, 0
+    while total_t < budget_s and pos < len(order):
+        ids = order[pos:pos + 16]
+        pos += len(ids)
+        idx = torch.tensor(ids, dtype=torch.long, device=t.p.device)
+        args = [x[idx].cpu().numpy() for x in (t.p, t.q, t.draft, t.u_accept, t.u_sample)]
+        t0 = time.perf_counter()
+        n, _ = BV.verify_block(*args)
+        total_t += time.perf_counter() - t0
+        emitted += int((n + 1).sum())
+        used += len(ids)
+    return {"value": per_seq * used / total_t / 1e9, "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "sample": f"block verification of {used} of {s.B} sequences (seeded choice)",
+            "seconds": round(total_t, 3), "tokens_per_s": emitted / total_t,
+            "tokens_unit": "emitted tokens/s"}
 
 
 def run_cpu_baseline_token(t: W.TokenInputs, budget_s: float):
@@ -702,10 +760,14 @@ def main():
     tok_bytes = None
     is_kvupd = isinstance(tk, W.KvUpdateInputs)
     is_fm = isinstance(tk, W.FeedbackInputs)
+    is_block = "block" in wl
     if is_fm:
         step, step_recorded, nbytes, tokens, tok_bytes = make_fm_step(tk)
     elif is_kvupd:
         step, step_recorded, nbytes, tokens, tok_bytes, _keep = make_kvupd_step(tk)
+    elif tk is not None and is_block:
+        step, step_recorded, nbytes, tokens, tau = make_block_step(tk)
+        tok_bytes = nbytes
     elif tk is not None:
         step, step_recorded, nbytes, tokens, tau = make_token_step(tk)
         tok_bytes = nbytes
@@ -733,8 +795,8 @@ def main():
     per_kernel_ms = recs
     kavg = {k: sum(x) / len(x) for k, x in recs.items()}
     # the dominant kernel is the attention kernel with the most time per step
-    partials = [k for k in ("verify_partial", "draft_partial", "token_weights", "draft_append",
-                            "kv_append", "draft_rollback", "feedback_memory") if k in recs]
+    partials = [k for k in ("verify_partial", "draft_partial", "token_weights", "block_weights",
+                            "draft_append", "kv_append", "draft_rollback", "feedback_memory") if k in recs]
     dominant = max(partials, key=lambda k: sum(recs[k]))
     dom_ms = kavg[dominant]
     dom_bytes = dominant_bytes(v, d, dominant, tok_bytes)
@@ -761,7 +823,8 @@ def main():
     elif tk is not None:
         spec = tk.spec
         cfg = {"workload": a.workload, "B": spec.B, "k": spec.k, "V": spec.V,
-               "prob_dtype": "f32", "mean_tokens_per_round": round(tau, 4)}
+               "prob_dtype": "f32", "mean_tokens_per_round": round(tau, 4),
+               "verification": "block" if is_block else "token"}
     else:
         spec = (v or d).spec
         cfg = {"workload": a.workload, "B": spec.B, "Hq": spec.Hq, "Hkv": spec.Hkv, "D": spec.D,
@@ -807,6 +870,8 @@ def main():
             res["cpu_baseline"] = run_cpu_baseline_fm(tk, a.cpu_seconds)
         elif is_kvupd:
             res["cpu_baseline"] = run_cpu_baseline_kvupd(tk, a.cpu_seconds)
+        elif tk is not None and is_block:
+            res["cpu_baseline"] = run_cpu_baseline_block(tk, a.cpu_seconds)
         elif tk is not None:
             res["cpu_baseline"] = run_cpu_baseline_token(tk, a.cpu_seconds)
         else:

@@ -153,6 +153,10 @@ def named_workloads():
         "verify_tp8shard_fp8_B512_k8": dict(
             verify=VerifySpec(B=512, Hq=8, Hkv=1, D=128, k=8, ctx_lo=2048, ctx_hi=65536,
                               kv_dtype="fp8", page_size=16, spare_pages=64)),
+        # block verification (the alternative to token verification, Sec. 6)
+        # on inputs drawn like the token verification workloads'
+        "block_verify_B256_k4_V128256": dict(block=TokenSpec(B=256, k=4, V=128256)),
+        "block_verify_B512_k8_V128256": dict(block=TokenSpec(B=512, k=8, V=128256)),
     }
 
 

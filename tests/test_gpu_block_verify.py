@@ -10,7 +10,6 @@ import pytest
 import torch
 
 from oracle import block_verify as BV
-from oracle import token_verify as TV
 from paper_2504_06419_amd import spire
 from paper_2504_06419_amd import workloads as W
 from tests.gpu_helpers import banner
@@ -49,10 +48,10 @@ def test_block_verify_small(k, V):
     _compare(W.make_token_inputs(spec, W.MASTER_SEED + 300 + k * 7 + V, device=DEV))
 
 
-@pytest.mark.parametrize("name", ["token_verify_B256_k4_V128256", "token_verify_B512_k8_V128256"])
+@pytest.mark.parametrize("name", ["block_verify_B256_k4_V128256", "block_verify_B512_k8_V128256"])
 def test_block_verify_full_workloads(name):
-    banner(f"block verify on the inputs of {name} (every sequence)")
-    spec = NW[name]["token"]
+    banner(f"block verify workload {name} (every sequence)")
+    spec = NW[name]["block"]
     inp = W.make_token_inputs(spec, W.MASTER_SEED + W.WORKLOAD_INDEX[name], device=DEV)
     n, _ = _compare(inp)
     assert 0 < n.mean() < spec.k
