@@ -389,11 +389,16 @@ int32_t spire_version(void);
  *                 0 automatic -- the matrix-core kernels where dtype and shape
  *                 allow (LDS-staged above 32 rows per KV head, register-staged
  *                 otherwise), the generic vector kernel for the rest;
+ *                 a draft step whose B * Hkv segments number half or a
+ *                 quarter of the device's waves (4 per compute unit; at least
+ *                 15/16 of them filled) gives each segment 2 or 4 waves of one
+ *                 workgroup and launches no plan or combine;
  *                 1 always the generic vector kernel; 2 prefer the
- *                 register-staged kernel (at most 32 rows); 3 prefer the
- *                 LDS-staged one (bf16 K/V only above 32 rows); each where its
- *                 limits allow.  Results agree within the stated tolerances;
- *                 the choice exists for measurement and cross-checks.
+ *                 register-staged kernel (at most 32 rows) with the stream-K
+ *                 partition of every call; 3 prefer the LDS-staged one (bf16
+ *                 K/V only above 32 rows); each where its limits allow.
+ *                 Results agree within the stated tolerances; the choice
+ *                 exists for measurement and cross-checks.
  *   max_launches  capacity of the two arrays below; 0 records nothing.
  *   events        host array [2 * max_launches] of events the CALLER created
  *                 (hipEventCreate, timing enabled) on the stream's device:

@@ -24,9 +24,10 @@
 //     8 keys x 8 dims in registers (byte permutes), and ends up owning the 32
 //     contiguous output dims 32j .. 32j + 31 of its row.
 //   * K: each load instruction covers 64 contiguous bytes of 16 key rows.
-// fp8 (OCP e4m3fn) K/V are converted to bf16 in registers (exact); the
-// per-head K scale is folded into the softmax scale, the V scale into the
-// final normalisation.
+// fp8 (OCP e4m3fn) K/V are converted in registers (exact): K to bf16 for the
+// QK product with the bf16 queries, V to fp16 for the PV product, whose P
+// operand then rounds to fp16 (bf16 K/V keep bf16 P); the per-head K scale
+// is folded into the softmax scale, the V scale into the final normalisation.
 //
 // This kernel serves up to 32 rows (NB <= 2): the query fragments stay in
 // registers and three tiles are kept in registers (two in flight).  More rows
@@ -34,6 +35,31 @@
 #include "mfma_common.h"
 
 namespace spire {
+
+// Tiles [first, last] of one segment through three register buffers, two
+// tiles in flight; only tiles of the range are loaded (a buffer is computed
+// only after its load).  The stream-K kernel below keeps the same loop
+// written out: as a call it compiled to a slightly different schedule.
+template <bool FP8, int NB, int MODE>
+__device__ __forceinline__ void stream_tiles(const SegAddr &a, const QFrag<NB, false> &qf,
+                                             SoftmaxState<NB, false> &st, int first, int last, int n,
+                                             int full_lim, float sc, int lane) {
+    TileRegs<FP8> A, Bt, C;
+    load_tile<FP8, MODE>(A, a, first, lane);
+    if (first + 1 <= last) load_tile<FP8, MODE>(Bt, a, first + 1, lane);
+    int tt = first;
+    while (true) {
+        if (tt + 2 <= last) load_tile<FP8, MODE>(C, a, tt + 2, lane);
+        compute_tile<FP8, NB>(A, qf, st, tt, n, full_lim, sc, lane);
+        if (++tt > last) break;
+        if (tt + 2 <= last) load_tile<FP8, MODE>(A, a, tt + 2, lane);
+        compute_tile<FP8, NB>(Bt, qf, st, tt, n, full_lim, sc, lane);
+        if (++tt > last) break;
+        if (tt + 2 <= last) load_tile<FP8, MODE>(Bt, a, tt + 2, lane);
+        compute_tile<FP8, NB>(C, qf, st, tt, n, full_lim, sc, lane);
+        if (++tt > last) break;
+    }
+}
 
 template <bool FP8, int NB, int MODE>
 __global__ __launch_bounds__(256, 1) void mfma_partial_kernel(Problem p, Plan pl) {
@@ -115,6 +141,107 @@ __global__ __launch_bounds__(256, 1) void mfma_partial_kernel(Problem p, Plan pl
         ++seg;
         tile = 0;
     }
+}
+
+// Whole draft segments per workgroup.  A draft segment never holds more than
+// S + W keys (paper Sec. 3.1: the constant-size sink + window cache), so when
+// the segments number half or a quarter of the device's waves, G = 2 or 4
+// waves of one workgroup per segment balance the work as the stream-K
+// partition does, without its seams: the waves split the segment's tiles
+// evenly (the short sink tile, last in the draft key space, goes to the last
+// wave), merge their rows through LDS and write the final rows -- no
+// partition, no partial slots, no combine launch.  Rows are merged on the
+// base-2 reference maxima: O = sum_w 2^(m_w - M) O_w, l = sum_w 2^(m_w - M) l_w
+// with M the largest reference; a wave that saw no finite score holds none
+// and weighs zero (its zero or NaN state still propagates).
+template <bool FP8, int NB, int G>
+__global__ __launch_bounds__(256, 1) void mfma_draft_coop_kernel(Problem p) {
+    static_assert(G >= 2 && kMfmaWavesPerWG % G == 0, "waves per segment");
+    constexpr int SPW = kMfmaWavesPerWG / G;  // segments per workgroup
+    __shared__ f32x4 s_acc[SPW][G - 1][8 * NB][64];
+    __shared__ float s_l[SPW][G - 1][NB][64];
+    __shared__ float s_m[SPW][G - 1][NB][64];  // reference maximum; -inf: none
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const int slot = wave / G, part = wave - (wave / G) * G;
+    const int seg = __builtin_amdgcn_readfirstlane((int)blockIdx.x * SPW + slot);
+    const bool valid = seg < p.B * p.Hkv;
+    const int b = valid ? seg / p.Hkv : 0;
+    const int h = valid ? seg - b * p.Hkv : 0;
+    SoftmaxState<NB, false> st;
+    if (valid) {
+        const int n = effective_keys(p, b);
+        const int T = (n + kMfmaTile - 1) / kMfmaTile;
+        const int t0 = part * T / G, t1 = (part + 1) * T / G;
+        const SegAddr a = make_seg_addr<MODE_DRAFT>(p, b, h, n);
+        QFrag<NB, false> qf;
+        begin_rows<FP8, NB, false, false>(p, b, h, n, 0, qf, st, lane);
+        float sc = p.sm_scale_log2;
+        if (FP8) sc *= uload(p.kv.k_scale, h);
+        if (t0 < t1) stream_tiles<FP8, NB, MODE_DRAFT>(a, qf, st, t0, t1 - 1, n, n, sc, lane);
+    }
+    if (valid && part > 0) {
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) {
+            float l = st.l[nb];
+            l += __shfl_xor(l, 16);
+            l += __shfl_xor(l, 32);
+            s_l[slot][part - 1][nb][lane] = l;
+            s_m[slot][part - 1][nb][lane] = st.thr[nb] == -INFINITY ? -INFINITY : st.msub[nb];
+#pragma unroll
+            for (int mb = 0; mb < 8; ++mb) s_acc[slot][part - 1][mb * NB + nb][lane] = st.acc[mb][nb];
+        }
+    }
+    __syncthreads();
+    if (!valid || part > 0) return;
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+        float l = st.l[nb];
+        l += __shfl_xor(l, 16);
+        l += __shfl_xor(l, 32);
+        const float m0 = st.thr[nb] == -INFINITY ? -INFINITY : st.msub[nb];
+        float M = m0;
+#pragma unroll
+        for (int w = 0; w < G - 1; ++w) M = fmaxf(M, s_m[slot][w][nb][lane]);
+        M = M == -INFINITY ? 0.f : M;
+        const float a0 = m0 == -INFINITY ? 0.f : fast_exp2(m0 - M);
+        l *= a0;
+#pragma unroll
+        for (int mb = 0; mb < 8; ++mb) st.acc[mb][nb] *= a0;
+#pragma unroll
+        for (int w = 0; w < G - 1; ++w) {
+            const float mw = s_m[slot][w][nb][lane];
+            const float aw = mw == -INFINITY ? 0.f : fast_exp2(mw - M);
+            l += s_l[slot][w][nb][lane] * aw;
+#pragma unroll
+            for (int mb = 0; mb < 8; ++mb) st.acc[mb][nb] += s_acc[slot][w][mb * NB + nb][lane] * aw;
+        }
+        st.msub[nb] = M;
+        // end_rows sums the four lane groups' partial row sums: one holds it all
+        st.l[nb] = (lane >> 4) == 0 ? l : 0.f;
+    }
+    end_rows<FP8, NB, false>(p, Plan{}, st, b, h, 0, true, 0, lane);
+}
+
+template <bool FP8, int NB>
+static hipError_t launch_coop_nb(const Problem &p, int g, hipStream_t st) {
+    const int segs = p.B * p.Hkv;
+    const dim3 block(64 * kMfmaWavesPerWG);
+    if (g == 4)
+        hipLaunchKernelGGL((mfma_draft_coop_kernel<FP8, NB, 4>), dim3(segs), block, 0, st, p);
+    else if (g == 2)
+        hipLaunchKernelGGL((mfma_draft_coop_kernel<FP8, NB, 2>), dim3((segs + 1) / 2), block, 0, st, p);
+    else
+        return hipErrorInvalidValue;
+    return hipGetLastError();
+}
+
+hipError_t launch_mfma_draft_coop(const Problem &p, int nb, int g, hipStream_t st) {
+    const bool fp8 = p.kv_dtype == SPIRE_FP8_E4M3FN;
+    if (!p.draft || p.B * p.Hkv <= 0) return hipErrorInvalidValue;
+    if (nb == 1) return fp8 ? launch_coop_nb<true, 1>(p, g, st) : launch_coop_nb<false, 1>(p, g, st);
+    if (nb == 2) return fp8 ? launch_coop_nb<true, 2>(p, g, st) : launch_coop_nb<false, 2>(p, g, st);
+    return hipErrorInvalidValue;
 }
 
 template <bool FP8, int NB>

@@ -14,9 +14,10 @@
 //     The LDS-staged fp8 kernel instead reads V^T transposed from LDS: row m
 //     of dim block mb' is head dim 16 mb' + m, and lane l owns output dims
 //     16 mb' + 4j .. 16 mb' + 4j + 3 of every block mb'.
-// fp8 (OCP e4m3fn) K/V are converted to bf16 in registers (exact); the
-// per-head K scale is folded into the softmax scale, the V scale into the
-// final normalisation.
+// fp8 (OCP e4m3fn) K/V are converted in registers (exact): K to bf16 for the
+// QK product with the bf16 queries, V to fp16 for the PV product, whose P
+// operand then rounds to fp16 (bf16 K/V keep bf16 P); the per-head K scale
+// is folded into the softmax scale, the V scale into the final normalisation.
 #pragma once
 
 #include <float.h>
@@ -30,6 +31,8 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x8 __attribute__((__vector_size__(16)));
 typedef __bf16 bf16x2 __attribute__((__vector_size__(4)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
 
 enum { MODE_CONTIG = 0, MODE_PAGED = 1, MODE_DRAFT = 2 };
 
@@ -72,10 +75,45 @@ __device__ __forceinline__ u32x4 fp8x8_to_bf16x8(uint32_t a, uint32_t b) {
     r.w = fp8x2_to_bf16x2<true>(b);
     return r;
 }
+// the same to fp16: every e4m3fn value (subnormals included, |x| <= 448) is
+// exact in fp16
+template <bool HI>
+__device__ __forceinline__ uint32_t fp8x2_to_f16x2(uint32_t x) {
+    return __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(x, 1.0f, HI));
+}
+__device__ __forceinline__ u32x4 fp8x8_to_f16x8(uint32_t a, uint32_t b) {
+    u32x4 r;
+    r.x = fp8x2_to_f16x2<false>(a);
+    r.y = fp8x2_to_f16x2<true>(a);
+    r.z = fp8x2_to_f16x2<false>(b);
+    r.w = fp8x2_to_f16x2<true>(b);
+    return r;
+}
 
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
     bf16x2 v = {(__bf16)lo, (__bf16)hi};
     return __builtin_bit_cast(uint32_t, v);
+}
+__device__ __forceinline__ uint32_t pack_f16x2(float lo, float hi) {
+    f16x2 v = {(_Float16)lo, (_Float16)hi};
+    return __builtin_bit_cast(uint32_t, v);
+}
+__device__ __forceinline__ f32x4 mfma_f16(u32x4 a, u32x4 b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, a),
+                                                  __builtin_bit_cast(f16x8, b), c, 0, 0, 0);
+}
+
+// The PV product's operand type.  With fp8 K/V it is fp16: the values convert
+// exactly and P keeps 11 significant bits (relative rounding error <= 2^-11;
+// P <= 2^8 by the lazy reference maximum, far inside fp16's range).  With bf16
+// K/V it is bf16, the values' own type (fp16 could not hold every bf16 value).
+template <bool F16>
+__device__ __forceinline__ uint32_t pack_p(float lo, float hi) {
+    return F16 ? pack_f16x2(lo, hi) : pack_bf16x2(lo, hi);
+}
+template <bool F16>
+__device__ __forceinline__ f32x4 mfma_pv(u32x4 a, u32x4 b, f32x4 c) {
+    return F16 ? mfma_f16(a, b, c) : mfma_bf16(a, b, c);
 }
 
 // K/V rows are streamed once: nontemporal loads (the streaming cache policy)
@@ -238,8 +276,9 @@ __device__ __forceinline__ float max8(f32x4 a, f32x4 b) {
                                          max3n(a[3], b[0], max3n(b[1], b[2], b[3])));
 }
 
-// bf16 1.0 in both halves: the A operand whose product with P^T is the row sum
+// 1.0 in both halves (bf16, fp16): the A operand whose product with P^T is the row sum
 constexpr uint32_t kOnesBF16x2 = 0x3F803F80u;
+constexpr uint32_t kOnesF16x2 = 0x3C003C00u;
 
 // 2^x with the hardware instruction: no denormal results (they would stand for
 // probabilities below 2^-126 of the row maximum and are dropped).
@@ -349,10 +388,10 @@ __device__ __forceinline__ void compute_tile(TileRegs<FP8> &T, const QFrag<NB, Q
         if constexpr (!LS)
             st.l[nb] += ((p[0][0] + p[0][1]) + (p[0][2] + p[0][3])) +
                         ((p[1][0] + p[1][1]) + (p[1][2] + p[1][3]));
-        pb[nb].x = pack_bf16x2(p[0][0], p[0][1]);
-        pb[nb].y = pack_bf16x2(p[0][2], p[0][3]);
-        pb[nb].z = pack_bf16x2(p[1][0], p[1][1]);
-        pb[nb].w = pack_bf16x2(p[1][2], p[1][3]);
+        pb[nb].x = pack_p<FP8>(p[0][0], p[0][1]);
+        pb[nb].y = pack_p<FP8>(p[0][2], p[0][3]);
+        pb[nb].z = pack_p<FP8>(p[1][0], p[1][1]);
+        pb[nb].w = pack_p<FP8>(p[1][2], p[1][3]);
     }
 
     // ---- V: keys beyond the segment end are zeroed (storage there may be anything)
@@ -371,13 +410,13 @@ __device__ __forceinline__ void compute_tile(TileRegs<FP8> &T, const QFrag<NB, Q
             for (int mb = 0; mb < 8; ++mb) T.v[mb] = u32x2{T.v[mb].x & m0, T.v[mb].y & m1};
         }
 #pragma unroll
-        for (int mb = 0; mb < 8; ++mb) vb[mb] = fp8x8_to_bf16x8(T.v[mb].x, T.v[mb].y);
+        for (int mb = 0; mb < 8; ++mb) vb[mb] = fp8x8_to_f16x8(T.v[mb].x, T.v[mb].y);
     } else {
 #pragma unroll
         for (int t = 0; t < 8; ++t) {
             if (FP8) {
                 const u32x2 raw = *reinterpret_cast<const u32x2 *>(&T.v[t]);
-                vb[t] = fp8x8_to_bf16x8(raw.x, raw.y);
+                vb[t] = fp8x8_to_f16x8(raw.x, raw.y);
             } else {
                 vb[t] = *reinterpret_cast<const u32x4 *>(&T.v[t]);
             }
@@ -390,7 +429,7 @@ __device__ __forceinline__ void compute_tile(TileRegs<FP8> &T, const QFrag<NB, Q
     }
 
     // ---- O^T += V^T P^T, row sums += 1^T P^T ---------------------------------
-    // Transpose 8 keys x 8 dims of bf16 with byte permutes: element t of
+    // Transpose 8 keys x 8 dims of 16-bit values with byte permutes: element t of
     // operand mb' is dim mb' (half mb'&1 of dword mb'>>1) of key t.
 #pragma unroll
     for (int mb = 0; mb < 8; ++mb) {
@@ -406,12 +445,13 @@ __device__ __forceinline__ void compute_tile(TileRegs<FP8> &T, const QFrag<NB, Q
             a.w = __builtin_amdgcn_perm(vb[7][w], vb[6][w], sel);
         }
 #pragma unroll
-        for (int nb = 0; nb < NB; ++nb) st.acc[mb][nb] = mfma_bf16(a, pb[nb], st.acc[mb][nb]);
+        for (int nb = 0; nb < NB; ++nb) st.acc[mb][nb] = mfma_pv<FP8>(a, pb[nb], st.acc[mb][nb]);
     }
     if constexpr (LS) {
-        const u32x4 ones = u32x4{kOnesBF16x2, kOnesBF16x2, kOnesBF16x2, kOnesBF16x2};
+        constexpr uint32_t one2 = FP8 ? kOnesF16x2 : kOnesBF16x2;
+        const u32x4 ones = u32x4{one2, one2, one2, one2};
 #pragma unroll
-        for (int nb = 0; nb < NB; ++nb) st.lsum[nb] = mfma_bf16(ones, pb[nb], st.lsum[nb]);
+        for (int nb = 0; nb < NB; ++nb) st.lsum[nb] = mfma_pv<FP8>(ones, pb[nb], st.lsum[nb]);
     }
 }
 

@@ -247,6 +247,20 @@ bool use_staged(const Problem &p, int kernel) {
     return false;  // measured: up to 32 rows the register-staged kernel is faster
 }
 
+// Waves per segment for a draft step with whole segments per workgroup, or 0
+// for the stream-K partition: 4 or 2 waves per segment when that fills at
+// least 15/16 of the device's waves without exceeding them (a draft segment
+// never exceeds S + W keys, so equal shares of segments stay balanced).
+// Kernel choice 2 keeps the stream-K partition.
+int draft_coop_waves(const Problem &p, int cus, int kernel) {
+    if (!p.draft || kernel == 2) return 0;
+    const int64_t segs = (int64_t)p.B * p.Hkv, waves = mfma_workers(cus);
+    if (segs <= 0) return 0;
+    for (int g = kMfmaWavesPerWG; g >= 2; g /= 2)
+        if (segs * g <= waves && segs * g * 16 >= waves * 15) return g;
+    return 0;
+}
+
 spire_status run(Problem &p, bool use_mfma, void *workspace, size_t ws_bytes, hipStream_t stream,
                  int partial_id, const spire_launch_opts *opts, bool lib_scratch = false) {
     int cus = 0;
@@ -288,9 +302,14 @@ spire_status run(Problem &p, bool use_mfma, void *workspace, size_t ws_bytes, hi
     pl.part_lse = reinterpret_cast<float *>(ws + L.part_lse);
     pl.part_o = reinterpret_cast<float *>(ws + L.part_o);
 
+    hipError_t e = hipSuccess;
+    if (const int g = (mf && !staged) ? draft_coop_waves(p, cus, kernel) : 0) {
+        e = rec.run(partial_id, stream, [&] { return launch_mfma_draft_coop(p, nb, g, stream); });
+        if (e != hipSuccess) return fail(SPIRE_ERR_HIP, "attention launch: %s", hipGetErrorString(e));
+        return SPIRE_OK;
+    }
     // the register-staged kernel computes the partition itself; the others
     // read it from the plan kernel's output
-    hipError_t e = hipSuccess;
     if (!mf || staged) {
         e = rec.run(KID_PLAN, stream, launch_plan, p, pl);
         if (e != hipSuccess) return fail(SPIRE_ERR_HIP, "plan launch: %s", hipGetErrorString(e));

@@ -159,6 +159,9 @@ __device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
 // ---- host-side launchers (one per kernel family) ---------------------------
 hipError_t launch_plan(const Problem &p, const Plan &pl, hipStream_t st);
 hipError_t launch_mfma_partial(const Problem &p, const Plan &pl, int nb, hipStream_t st);
+// Draft steps with whole segments per workgroup (g = 2 or 4 waves per segment):
+// final rows written directly, no plan and no combine.
+hipError_t launch_mfma_draft_coop(const Problem &p, int nb, int g, hipStream_t st);
 hipError_t launch_generic_partial(const Problem &p, const Plan &pl, hipStream_t st);
 hipError_t launch_staged_partial(const Problem &p, const Plan &pl, int nb, hipStream_t st);
 // LDS-staged kernel: waves per worker (a workgroup), waves per SIMD, and the
